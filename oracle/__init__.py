@@ -57,6 +57,7 @@ def lib():
         L.cbref_num_tensors.argtypes = [_P]
         L.cbref_tensor_info.argtypes = [_P, ctypes.c_int, _P, _P, _P, _P]
         L.cbref_learner_grad.argtypes = [_P, _P, _P, _P, ctypes.c_int, _P, _P]
+        L.cbref_learner_margin.argtypes = [_P, _P, _P, _P, ctypes.c_int, _P, _P]
         L.cbref_create.restype = _P
         L.cbref_create.argtypes = [_P, _P, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_double, ctypes.c_double, ctypes.c_double,
@@ -78,6 +79,11 @@ def lib():
                                       _P, _P, _P, _P]
         L.cbref_maxpool.argtypes = [_P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_int, ctypes.c_int, _P, _P, _P]
+        L.cbref_sma_update.argtypes = [ctypes.c_int, ctypes.c_int64, _P, _P, _P, _P, _P,
+                                       ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                       ctypes.c_double, ctypes.c_int]
+        L.cbref_conv_samples.argtypes = [ctypes.c_int, _P, _P, _P, _P] + [ctypes.c_int] * 8 + [
+            _P, ctypes.c_int, _P]
         L.cbref_softmax_xent.restype = ctypes.c_double
         L.cbref_softmax_xent.argtypes = [_P, _P, ctypes.c_int, ctypes.c_int, _P]
         _lib = L
@@ -128,6 +134,22 @@ def learner_grad(m: Model, w, x, y, want_grad: bool = True):
     if rc:
         raise ValueError("cbref_learner_grad failed")
     return loss.value, g
+
+
+def learner_margin(m: Model, w, x, y, with_bn=False):
+    """Smallest relative distance of any ReLU input, or any max-pool winner
+    from its runner-up, to the point where that decision flips (forward
+    pass of one learner's batch, relative to the layer's RMS).  With
+    with_bn, also the largest batch-norm conditioning factor."""
+    w = _f64(w)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    out, cond = ctypes.c_double(), ctypes.c_double()
+    rc = lib().cbref_learner_margin(ctypes.byref(m), _ptr(w), _ptr(x), _ptr(y), len(y),
+                                    ctypes.byref(out), ctypes.byref(cond))
+    if rc:
+        raise ValueError("cbref_learner_margin failed")
+    return (out.value, cond.value) if with_bn else out.value
 
 
 class SMA:
@@ -244,3 +266,32 @@ def softmax_xent(logits, y):
     d = np.empty_like(o)
     loss = lib().cbref_softmax_xent(_ptr(o), _ptr(y), o.shape[0], o.shape[1], _ptr(d))
     return loss, d
+
+
+def sma_update(W, G, Z, Zp, alpha, lr, mu, mu_l=0.0, Wprev=None, correct=True):
+    """One synchronisation of Algorithm 1 on [k][n] replicas; returns new
+    (W, Wprev, Z, Zp) as float64 arrays (inputs are not modified)."""
+    W = np.array(W, dtype=np.float64, order="C")
+    k = W.shape[0]
+    n = W.shape[1]
+    Wp = W.copy() if Wprev is None else np.array(Wprev, dtype=np.float64, order="C")
+    G = _f64(G).reshape(k, n)
+    Z = np.array(Z, dtype=np.float64)
+    Zp = np.array(Zp, dtype=np.float64)
+    lib().cbref_sma_update(k, n, _ptr(W), _ptr(Wp), _ptr(G), _ptr(Z), _ptr(Zp), float(alpha),
+                           float(lr), float(mu), float(mu_l), 1 if correct else 0)
+    return W, Wp, Z, Zp
+
+
+def conv_samples(what, q, x=None, dy=None, w=None, bias=None, *, N, Ci, H, W, Co, R, stride, pad):
+    """Conv output (what=0), weight gradient (1) or input gradient (2) at the
+    index quadruples q [n, 4], each from the definition.  Arrays are fp32
+    (one replica: x [N][Ci][H][W], dy [N][Co][Ho][Wo], w [Co][Ci][R][R])."""
+    def f32(a):
+        return None if a is None else np.ascontiguousarray(a, dtype=np.float32)
+    q = np.ascontiguousarray(q, dtype=np.int32).reshape(-1, 4)
+    out = np.empty(len(q))
+    x, dy, w, bias = f32(x), f32(dy), f32(w), f32(bias)
+    lib().cbref_conv_samples(what, _ptr(x), _ptr(dy), _ptr(w), _ptr(bias), N, Ci, H, W, Co, R,
+                             stride, pad, _ptr(q), len(q), _ptr(out))
+    return out

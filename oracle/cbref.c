@@ -251,6 +251,24 @@ static int build_net(const cbref_model* m, Net* n) {
 /* Layer math (Sec. 2.1: forward pass, loss, backward pass)            */
 /* ------------------------------------------------------------------ */
 
+/* Decision margin: the smallest distance, relative to the layer's RMS, of
+ * any value on which a ReLU or a max-pool decision turns.  A decision whose
+ * margin is within rounding can go either way in another precision; the
+ * tests use this to know which inputs make every decision unambiguous.
+ * Single-threaded oracle: one running minimum, reset by the API. */
+static double g_margin = INFINITY;
+
+static void note_margin(double m) {
+  if (m < g_margin) g_margin = m;
+}
+
+/* Batch-norm conditioning: the largest, over channels, of
+ * sqrt(var + mean^2) / sqrt(var + eps), the factor by which a relative
+ * error in the norm's input grows in its output.  Over very few values a
+ * channel can have a spread far below its mean, and then fp32 inputs carry
+ * little of the normalised output's precision. */
+static double g_bn_cond = 0.0;
+
 static double* dalloc(size_t n) {
   double* p = (double*)calloc(n ? n : 1, sizeof(double));
   if (!p) abort();
@@ -420,6 +438,8 @@ static void bn_fwd(const BN* b, const double* w, const double* x, int N, int HW,
     }
     v /= cnt;
     double is = 1.0 / sqrt(v + BN_EPS);
+    double cond = sqrt(v + mu * mu) * is;
+    if (cond > g_bn_cond) g_bn_cond = cond;
     double ga = w[b->g_off + c], be = w[b->b_off + c];
     for (int n = 0; n < N; ++n) {
       const double* p = x + ((size_t)n * b->c + c) * HW;
@@ -463,7 +483,15 @@ static void bn_bwd(const BN* b, const double* w, const double* x, int N, int HW,
   }
 }
 
+
+
 static void relu_inplace(double* y, size_t n) {
+  double ss = 0.0, mn = INFINITY;
+  for (size_t i = 0; i < n; ++i) {
+    ss += y[i] * y[i];
+    if (fabs(y[i]) < mn) mn = fabs(y[i]);
+  }
+  if (n && ss > 0.0) note_margin(mn / sqrt(ss / n));
   for (size_t i = 0; i < n; ++i)
     if (!(y[i] > 0.0)) y[i] = 0.0;
 }
@@ -479,6 +507,8 @@ static void relu_mask(double* dy, const double* out, size_t n) {
  * greater than every earlier one; padded cells never win. */
 static void maxpool_fwd(const double* x, int N, int C, int H, int W, int K, int st, int pad,
                         double* y, int Ho, int Wo, int* arg) {
+  double ss = 0.0, gap = INFINITY;
+  for (size_t i = 0; i < (size_t)N * C * H * W; ++i) ss += x[i] * x[i];
   for (size_t nc = 0; nc < (size_t)N * C; ++nc)
     for (int oh = 0; oh < Ho; ++oh)
       for (int ow = 0; ow < Wo; ++ow) {
@@ -496,7 +526,19 @@ static void maxpool_fwd(const double* x, int N, int C, int H, int W, int K, int 
           }
         y[nc * Ho * Wo + oh * Wo + ow] = x[nc * H * W + best];
         arg[nc * Ho * Wo + oh * Wo + ow] = best;
+        /* margin: gap to the runner-up, when the winner is positive (a
+         * non-positive winner's gradient is cut by the ReLU before it) */
+        if (bv > 0.0f)
+          for (int r = 0; r < K; ++r)
+            for (int s = 0; s < K; ++s) {
+              int ih = oh * st - pad + r, iw = ow * st - pad + s;
+              if (ih < 0 || ih >= H || iw < 0 || iw >= W || ih * W + iw == best) continue;
+              double d = x[nc * H * W + best] - x[nc * H * W + ih * W + iw];
+              if (d < gap) gap = d;
+            }
       }
+  size_t n = (size_t)N * C * H * W;
+  if (n && ss > 0.0 && gap < INFINITY) note_margin(gap / sqrt(ss / n));
 }
 
 static void maxpool_bwd(const double* dy, const int* arg, int N, int C, int H, int W, int Ho,
@@ -884,6 +926,21 @@ int cbref_learner_grad(const cbref_model* m, const double* w, const float* x,
   return 0;
 }
 
+/* Smallest relative decision margin of the forward pass of one learner's
+ * batch (see g_margin) and, if bn_cond is not NULL, its largest batch-norm
+ * conditioning factor (see g_bn_cond).  Returns 0, or -1 on a bad model or
+ * label. */
+int cbref_learner_margin(const cbref_model* m, const double* w, const float* x,
+                         const int32_t* y, int N, double* margin, double* bn_cond) {
+  double loss;
+  g_margin = INFINITY;
+  g_bn_cond = 0.0;
+  int rc = cbref_learner_grad(m, w, x, y, N, NULL, &loss);
+  *margin = g_margin;
+  if (bn_cond) *bn_cond = g_bn_cond;
+  return rc;
+}
+
 /* ------------------------------------------------------------------ */
 /* Synchronous model averaging (Algorithm 1, Sec. 3.2)                 */
 /* ------------------------------------------------------------------ */
@@ -929,23 +986,31 @@ void cbref_destroy(cbref_ctx* c) {
   free(c);
 }
 
-/* The replica update of Algorithm 1 with the correction taken against z:
- * w_j <- w_j - lr*g_j - alpha*(w_j - z) + mu_L*(w_j - w_j_prev).
- * With correct == 0 the correction term is left out (a local step). */
-static void replica_update(cbref_ctx* c, int correct, double* S) {
-  int64_t P = c->P;
-  for (int64_t e = 0; e < P; ++e) {
+/* One synchronisation of Algorithm 1 on n parameters of k replicas held as
+ * [k][n] arrays (W, Wprev, G) and [n] arrays (Z, Zp):
+ *   c_j = alpha (w_j - z)            from the replica before its update,
+ *   w_j <- w_j - lr g_j - c_j + mu_L (w_j - w_j_prev),   w_j_prev <- old w_j,
+ *   z <- z + sum_j c_j + mu (z - z_prev),                z_prev <- old z,
+ * the sum taken in replica order.  With correct == 0 the correction is left
+ * out and z is not touched (a local step of a learner). */
+void cbref_sma_update(int k, int64_t n, double* W, double* Wprev, const double* G, double* Z,
+                      double* Zp, double alpha, double lr, double mu, double mu_l, int correct) {
+  for (int64_t e = 0; e < n; ++e) {
     double s = 0.0;
-    for (int j = 0; j < c->k; ++j) {
-      size_t i = (size_t)j * P + e;
-      double w = c->W[i];
-      double cj = correct ? c->alpha * (w - c->Z[e]) : 0.0;
-      double wn = w - c->lr * c->G[i] - cj + c->mu_l * (w - c->Wprev[i]);
-      c->Wprev[i] = w;
-      c->W[i] = wn;
+    for (int j = 0; j < k; ++j) {
+      size_t i = (size_t)j * n + e;
+      double w = W[i];
+      double cj = correct ? alpha * (w - Z[e]) : 0.0;
+      double wn = w - lr * G[i] - cj + mu_l * (w - Wprev[i]);
+      Wprev[i] = w;
+      W[i] = wn;
       s += cj;
     }
-    if (S) S[e] = s;
+    if (correct) {
+      double z = Z[e];
+      Z[e] = z + s + mu * (z - Zp[e]);
+      Zp[e] = z;
+    }
   }
 }
 
@@ -954,7 +1019,9 @@ static void replica_update(cbref_ctx* c, int correct, double* S) {
  * from an earlier step() that was never synchronised is applied first as
  * a local step. */
 int cbref_step(cbref_ctx* c, const float* x, const int32_t* y) {
-  if (c->pending) replica_update(c, 0, NULL);
+  if (c->pending)
+    cbref_sma_update(c->k, c->P, c->W, c->Wprev, c->G, c->Z, c->Zp, c->alpha, c->lr, c->mu,
+                     c->mu_l, 0);
   const cbref_model* m = &c->net.m;
   size_t img = (size_t)m->in_c * m->in_h * m->in_w;
   for (int j = 0; j < c->k; ++j) {
@@ -973,14 +1040,8 @@ int cbref_step(cbref_ctx* c, const float* x, const int32_t* y) {
  * and z_prev <- the old z.  Returns -4 if no gradient is pending. */
 int cbref_sync(cbref_ctx* c) {
   if (!c->pending) return -4;
-  double* S = dalloc(c->P);
-  replica_update(c, 1, S);
-  for (int64_t e = 0; e < c->P; ++e) {
-    double z = c->Z[e];
-    c->Z[e] = z + S[e] + c->mu * (z - c->Zp[e]);
-    c->Zp[e] = z;
-  }
-  free(S);
+  cbref_sma_update(c->k, c->P, c->W, c->Wprev, c->G, c->Z, c->Zp, c->alpha, c->lr, c->mu,
+                   c->mu_l, 1);
   c->pending = 0;
   return 0;
 }
@@ -1081,6 +1142,62 @@ void cbref_maxpool(const double* x, int N, int C, int H, int W, int K, int st, i
   maxpool_fwd(x, N, C, H, W, K, st, pad, y, Ho, Wo, arg);
   if (dy) maxpool_bwd(dy, arg, N, C, H, W, Ho, Wo, dx);
   free(arg);
+}
+
+/* Sampled elements of a convolution and its gradients, each computed
+ * alone from the definition (for checks at sizes where the full tensors
+ * are too slow).  Inputs are fp32 as stored; sums run in double.
+ *   what 0: y[n][co][oh][ow]  = bias[co] + sum_(ci,r,s) x * w     (q = n,co,oh,ow)
+ *   what 1: dW[co][ci][r][s]  = sum_(n,oh,ow) dy * x               (q = co,ci,r,s)
+ *   what 2: dX[n][ci][ih][iw] = sum_(co,r,s) dy * w over the taps
+ *           with oh*st = ih + pad - r, ow*st = iw + pad - s        (q = n,ci,ih,iw)
+ * q holds 4 indices per sample. */
+void cbref_conv_samples(int what, const float* x, const float* dy, const float* w,
+                        const float* bias, int N, int Ci, int H, int W, int Co, int R, int st,
+                        int pad, const int32_t* q, int nsamples, double* out) {
+  int Ho = out_dim(H, R, st, pad), Wo = out_dim(W, R, st, pad);
+  for (int t = 0; t < nsamples; ++t) {
+    const int32_t* e = q + 4 * t;
+    double acc = 0.0;
+    if (what == 0) {
+      int n = e[0], co = e[1], oh = e[2], ow = e[3];
+      acc = bias ? bias[co] : 0.0;
+      for (int ci = 0; ci < Ci; ++ci)
+        for (int r = 0; r < R; ++r)
+          for (int s = 0; s < R; ++s) {
+            int ih = oh * st - pad + r, iw = ow * st - pad + s;
+            if (ih < 0 || ih >= H || iw < 0 || iw >= W) continue;
+            acc += (double)x[(((size_t)n * Ci + ci) * H + ih) * W + iw] *
+                   (double)w[(((size_t)co * Ci + ci) * R + r) * R + s];
+          }
+    } else if (what == 1) {
+      int co = e[0], ci = e[1], r = e[2], s = e[3];
+      for (int n = 0; n < N; ++n)
+        for (int oh = 0; oh < Ho; ++oh) {
+          int ih = oh * st - pad + r;
+          if (ih < 0 || ih >= H) continue;
+          for (int ow = 0; ow < Wo; ++ow) {
+            int iw = ow * st - pad + s;
+            if (iw < 0 || iw >= W) continue;
+            acc += (double)dy[(((size_t)n * Co + co) * Ho + oh) * Wo + ow] *
+                   (double)x[(((size_t)n * Ci + ci) * H + ih) * W + iw];
+          }
+        }
+    } else {
+      int n = e[0], ci = e[1], ih = e[2], iw = e[3];
+      for (int co = 0; co < Co; ++co)
+        for (int r = 0; r < R; ++r)
+          for (int s = 0; s < R; ++s) {
+            int th = ih + pad - r, tw = iw + pad - s;
+            if (th < 0 || tw < 0 || th % st || tw % st) continue;
+            int oh = th / st, ow = tw / st;
+            if (oh >= Ho || ow >= Wo) continue;
+            acc += (double)dy[(((size_t)n * Co + co) * Ho + oh) * Wo + ow] *
+                   (double)w[(((size_t)co * Ci + ci) * R + r) * R + s];
+          }
+    }
+    out[t] = acc;
+  }
 }
 
 double cbref_softmax_xent(const double* logits, const int32_t* y, int N, int C, double* dlogits) {

@@ -1,0 +1,619 @@
+// conv_gemm.hip -- replica-batched convolution (and FC) as implicit GEMM on
+// the fp32 matrix cores of gfx950 (v_mfma_f32_16x16x4f32).
+//
+// Sec. 2.1: training a learner is a forward pass and a backward pass
+// through its layers; for a convolution these are three contractions:
+//   forward      Y[m][n]  = sum_k A[m][k] W[n][k],  m=(img,oh,ow), n=co, k=(ci,r,s)
+//   data grad    dX[m][n] = sum_k dY~[m][k] W'[k][n], m=(img,ih,iw), n=ci, k=(co,r,s)
+//   weight grad  dW[n][k] = sum_m dY[m][n] A[m][k],  contracted over the
+//                                                      b*Ho*Wo pixels of a learner
+// Every learner has its own weights, so the grid's z axis runs over the k
+// replicas: one launch covers all learners and fills the CUs even when each
+// learner's batch is small (Sec. 3.1: learners train independently).
+//
+// Tiling: 256 threads (4 wave64s), LDS stages of BK = 16 contraction steps
+// stored with k contiguous, so each 16x16x4 MFMA operand group is one
+// ds_read_b128; the contraction index seen by lane l at sub-step kk is
+// 4*(l/16) + kk for both operands.  Global loads for the next stage are in
+// flight while the current stage is multiplied (two LDS buffers, one barrier
+// per stage).  The filter size R is a template parameter, so splitting a
+// contraction index into (channel, r, s) is multiply-shift arithmetic; in the
+// A-operand loaders that index is wave-uniform and the split runs on the
+// scalar unit.
+#include "kernels.hpp"
+
+#include <algorithm>
+#include <string>
+
+namespace cbk {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+constexpr int BK = 16;        // contraction steps per LDS stage
+constexpr int LDK = BK + 4;   // LDS row stride in floats (16-byte aligned rows)
+constexpr int OUT_OF_RANGE = -(1 << 29);
+
+__device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// One LDS stage: As[rows][LDK], Bs[cols][LDK], both k-contiguous.
+template <int TM, int TN>
+__device__ __forceinline__ void mma_stage(const float* As, const float* Bs, int wm0, int wn0,
+                                          int lane, v4f (&acc)[TM][TN]) {
+  const int r = lane & 15, q = (lane >> 4) * 4;
+  v4f av[TM], bv[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) av[i] = *reinterpret_cast<const v4f*>(As + (wm0 + i * 16 + r) * LDK + q);
+#pragma unroll
+  for (int i = 0; i < TN; ++i) bv[i] = *reinterpret_cast<const v4f*>(Bs + (wn0 + i * 16 + r) * LDK + q);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b) acc[a][b] = mfma4(av[a][kk], bv[b][kk], acc[a][b]);
+}
+
+__device__ __forceinline__ float relu0(float v) { return v > 0.f ? v : 0.f; }
+
+// ---------------------------------------------------------------- forward
+template <int BM, int BN, int WM, int WN, int R>
+__global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
+  constexpr int RS = R * R;
+  constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
+  constexpr int TPR = 256 / BM;   // threads sharing one output row
+  constexpr int KPT = BK / TPR;   // contraction steps each of them loads
+  constexpr int BQ = BN * (BK / 4);
+  constexpr int BPT = (BQ + 255) / 256;
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDK];
+
+  const ConvGeom g = a.g;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int j = blockIdx.z;
+  const int HW = g.H * g.W, HoWo = g.Ho * g.Wo;
+  const int M = g.b * HoWo, N = g.Co, K = g.Ci * RS;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const float* X = a.x + (int64_t)j * g.b * g.Ci * HW;
+  const float* Wt = a.w + (int64_t)j * a.pstride;
+
+  const int am = tid % BM;
+  const int akq = __builtin_amdgcn_readfirstlane(tid / BM);
+  int ih0 = OUT_OF_RANGE, iw0 = OUT_OF_RANGE, xb = 0;
+  {
+    const int m = m0 + am;
+    if (m < M) {
+      const int img = m / HoWo, p = m - img * HoWo, oh = p / g.Wo, ow = p - oh * g.Wo;
+      ih0 = oh * g.st - g.pad;
+      iw0 = ow * g.st - g.pad;
+      xb = img * g.Ci * HW + ih0 * g.W + iw0;
+    }
+  }
+  float ra[KPT];
+  float rb[BPT][4];
+
+  auto loadA = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int k = k0 + akq * KPT + i;  // wave-uniform
+      float v = 0.f;
+      if (k < K) {
+        const int ci = k / RS, rs = k - ci * RS, r = rs / R, s = rs - r * R;
+        if ((unsigned)(ih0 + r) < (unsigned)g.H && (unsigned)(iw0 + s) < (unsigned)g.W)
+          v = X[xb + ci * HW + r * g.W + s];
+      }
+      ra[i] = v;
+    }
+  };
+  auto loadB = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < BPT; ++u) {
+      const int idx = tid + u * 256, n = n0 + (idx >> 2), kq = k0 + 4 * (idx & 3);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        rb[u][i] = (idx < BQ && n < N && kq + i < K) ? Wt[(int64_t)n * K + kq + i] : 0.f;
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < KPT / 4; ++q)
+      *reinterpret_cast<v4f*>(&As[buf][am * LDK + akq * KPT + 4 * q]) =
+          v4f{ra[4 * q], ra[4 * q + 1], ra[4 * q + 2], ra[4 * q + 3]};
+#pragma unroll
+    for (int u = 0; u < BPT; ++u) {
+      const int idx = tid + u * 256;
+      if (idx < BQ)
+        *reinterpret_cast<v4f*>(&Bs[buf][(idx >> 2) * LDK + 4 * (idx & 3)]) =
+            v4f{rb[u][0], rb[u][1], rb[u][2], rb[u][3]};
+    }
+  };
+
+  v4f acc[TM][TN];
+#pragma unroll
+  for (int x = 0; x < TM; ++x)
+#pragma unroll
+    for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+  const int wm0 = (wave % WM) * TM * 16, wn0 = (wave / WM) * TN * 16;
+  const int T = (K + BK - 1) / BK;
+  loadA(0);
+  loadB(0);
+  store(0);
+  __syncthreads();
+  for (int t = 0; t < T; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < T) {
+      loadA((t + 1) * BK);
+      loadB((t + 1) * BK);
+    }
+    mma_stage<TM, TN>(As[cur], Bs[cur], wm0, wn0, lane, acc);
+    if (t + 1 < T) store(cur ^ 1);
+    __syncthreads();
+  }
+
+  const float* bias = a.bias ? a.bias + (int64_t)j * a.pstride : nullptr;
+  float* Y = a.y + (int64_t)j * g.b * N * HoWo;
+#pragma unroll
+  for (int x = 0; x < TM; ++x)
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+      const int n = n0 + wn0 + y * 16 + (lane & 15);
+      const int mb = m0 + wm0 + x * 16 + (lane >> 4) * 4;
+      if (n >= N || mb >= M) continue;
+      const float bv = bias ? bias[n] : 0.f;
+      int img = mb / HoWo, p = mb - img * HoWo;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (mb + i < M) {
+          float v = acc[x][y][i] + bv;
+          if (a.relu) v = relu0(v);
+          Y[((int64_t)img * N + n) * HoWo + p] = v;
+        }
+        if (++p == HoWo) {
+          p = 0;
+          ++img;
+        }
+      }
+    }
+}
+
+// ------------------------------------------------------------ data grad
+template <int BM, int BN, int WM, int WN, int R, int ST>
+__global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
+  constexpr int RS = R * R;
+  constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
+  constexpr int TPR = 256 / BM;
+  constexpr int KPT = BK / TPR;
+  constexpr int BQ = BN * (BK / 4);
+  constexpr int BPT = (BQ + 255) / 256;
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDK];
+
+  const ConvGeom g = a.g;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int j = blockIdx.z;
+  const int HW = g.H * g.W, HoWo = g.Ho * g.Wo;
+  const int M = g.b * HW, N = g.Ci, K = g.Co * RS;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const float* DY = a.dy + (int64_t)j * g.b * g.Co * HoWo;
+  const float* Wt = a.w + (int64_t)j * a.pstride;
+
+  const int am = tid % BM;
+  const int akq = __builtin_amdgcn_readfirstlane(tid / BM);
+  int thp = OUT_OF_RANGE, twp = OUT_OF_RANGE, yb = 0;
+  {
+    const int m = m0 + am;
+    if (m < M) {
+      const int img = m / HW, p = m - img * HW, ih = p / g.W, iw = p - ih * g.W;
+      thp = ih + g.pad;
+      twp = iw + g.pad;
+      yb = img * g.Co * HoWo;
+    }
+  }
+  float ra[KPT];
+  float rb[BPT][4];
+
+  auto loadA = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int k = k0 + akq * KPT + i;  // wave-uniform
+      float v = 0.f;
+      if (k < K) {
+        const int co = k / RS, rs = k - co * RS, r = rs / R, s = rs - r * R;
+        const int th = thp - r, tw = twp - s;
+        if (ST == 1) {
+          if ((unsigned)th < (unsigned)g.Ho && (unsigned)tw < (unsigned)g.Wo)
+            v = DY[yb + co * HoWo + th * g.Wo + tw];
+        } else {
+          if ((unsigned)th < (unsigned)(ST * g.Ho) && (unsigned)tw < (unsigned)(ST * g.Wo) &&
+              th % ST == 0 && tw % ST == 0)
+            v = DY[yb + co * HoWo + (th / ST) * g.Wo + tw / ST];
+        }
+      }
+      ra[i] = v;
+    }
+  };
+  auto loadB = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < BPT; ++u) {
+      const int idx = tid + u * 256, n = n0 + (idx >> 2), kq = k0 + 4 * (idx & 3);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float v = 0.f;
+        const int k = kq + i, co = k / RS, rs = k - co * RS;
+        if (idx < BQ && n < N && k < K) v = Wt[((int64_t)co * N + n) * RS + rs];
+        rb[u][i] = v;
+      }
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < KPT / 4; ++q)
+      *reinterpret_cast<v4f*>(&As[buf][am * LDK + akq * KPT + 4 * q]) =
+          v4f{ra[4 * q], ra[4 * q + 1], ra[4 * q + 2], ra[4 * q + 3]};
+#pragma unroll
+    for (int u = 0; u < BPT; ++u) {
+      const int idx = tid + u * 256;
+      if (idx < BQ)
+        *reinterpret_cast<v4f*>(&Bs[buf][(idx >> 2) * LDK + 4 * (idx & 3)]) =
+            v4f{rb[u][0], rb[u][1], rb[u][2], rb[u][3]};
+    }
+  };
+
+  v4f acc[TM][TN];
+#pragma unroll
+  for (int x = 0; x < TM; ++x)
+#pragma unroll
+    for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+  const int wm0 = (wave % WM) * TM * 16, wn0 = (wave / WM) * TN * 16;
+  const int T = (K + BK - 1) / BK;
+  loadA(0);
+  loadB(0);
+  store(0);
+  __syncthreads();
+  for (int t = 0; t < T; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < T) {
+      loadA((t + 1) * BK);
+      loadB((t + 1) * BK);
+    }
+    mma_stage<TM, TN>(As[cur], Bs[cur], wm0, wn0, lane, acc);
+    if (t + 1 < T) store(cur ^ 1);
+    __syncthreads();
+  }
+
+  float* DX = a.dx + (int64_t)j * g.b * N * HW;
+  const float* MSK = a.mask ? a.mask + (int64_t)j * g.b * N * HW : nullptr;
+  const int Hs = g.H / (a.add_st > 0 ? a.add_st : 1), Ws = g.W / (a.add_st > 0 ? a.add_st : 1);
+  const float* ADD = a.add;
+  if (ADD)
+    ADD += (a.add_mode == ADD_SAME) ? (int64_t)j * g.b * N * HW
+                                    : (int64_t)j * g.b * a.add_C * Hs * Ws;
+#pragma unroll
+  for (int x = 0; x < TM; ++x)
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+      const int n = n0 + wn0 + y * 16 + (lane & 15);
+      const int mb = m0 + wm0 + x * 16 + (lane >> 4) * 4;
+      if (n >= N || mb >= M) continue;
+      int img = mb / HW, p = mb - img * HW;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (mb + i < M) {
+          const int64_t idx = ((int64_t)img * N + n) * HW + p;
+          float v = acc[x][y][i];
+          if (a.accumulate) v += DX[idx];
+          if (a.add_mode == ADD_SAME) {
+            v += ADD[idx];
+          } else if (a.add_mode == ADD_SUBSAMPLE) {
+            const int ih = p / g.W, iw = p - ih * g.W;
+            if (ih % a.add_st == 0 && iw % a.add_st == 0)
+              v += ADD[(((int64_t)img * a.add_C + n) * Hs + ih / a.add_st) * Ws + iw / a.add_st];
+          }
+          if (MSK && !(MSK[idx] > 0.f)) v = 0.f;
+          DX[idx] = v;
+        }
+        if (++p == HW) {
+          p = 0;
+          ++img;
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------- weight grad
+template <int BM, int BN, int WM, int WN, int R>
+__global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
+  constexpr int RS = R * R;
+  constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
+  constexpr int RA = BM / 16, RB = BN / 16;  // rows each thread loads per stage
+  __shared__ __attribute__((aligned(16))) float As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDK];
+
+  const ConvGeom g = a.g;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int j = blockIdx.z / a.splits, split = blockIdx.z - j * a.splits;
+  const int HW = g.H * g.W, HoWo = g.Ho * g.Wo;
+  const int Mo = g.Co, No = g.Ci * RS, L = g.b * HoWo;
+  const int L0 = split * a.chunk, L1 = min(L, L0 + a.chunk);
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const float* X = a.x + (int64_t)j * g.b * g.Ci * HW;
+  const float* DY = a.dy + (int64_t)j * g.b * g.Co * HoWo;
+
+  const int pl = tid & 15, rg = tid >> 4;
+  // pixel this thread loads in the current stage, kept as (img, oh, ow)
+  int pix = L0 + pl;
+  int img = pix / HoWo, rem = pix - img * HoWo, oh = rem / g.Wo, ow = rem - oh * g.Wo;
+  // (offset, r, s) of this thread's weight-gradient columns kk = (ci, r, s)
+  int tx[RB], tr[RB], ts[RB];
+#pragma unroll
+  for (int i = 0; i < RB; ++i) {
+    const int kk = n0 + rg + 16 * i;
+    const int ci = kk / RS, rs = kk - ci * RS, r = rs / R, s = rs - r * R;
+    tx[i] = ci * HW + r * g.W + s;
+    tr[i] = kk < No ? r : OUT_OF_RANGE;
+    ts[i] = s;
+  }
+  float ra[RA], rb[RB];
+
+  auto load = [&]() {
+    const bool ok = pix < L1;
+    const int yb = img * g.Co * HoWo + oh * g.Wo + ow;
+    const int ih0 = oh * g.st - g.pad, iw0 = ow * g.st - g.pad;
+    const int xb = img * g.Ci * HW + ih0 * g.W + iw0;
+#pragma unroll
+    for (int i = 0; i < RA; ++i) {
+      const int co = m0 + rg + 16 * i;
+      ra[i] = (ok && co < Mo) ? DY[yb + co * HoWo] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      float v = 0.f;
+      if (ok && (unsigned)(ih0 + tr[i]) < (unsigned)g.H && (unsigned)(iw0 + ts[i]) < (unsigned)g.W)
+        v = X[xb + tx[i]];
+      rb[i] = v;
+    }
+  };
+  auto advance = [&]() {
+    pix += BK;
+    ow += BK;
+    while (ow >= g.Wo) {
+      ow -= g.Wo;
+      if (++oh == g.Ho) {
+        oh = 0;
+        ++img;
+      }
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < RA; ++i) As[buf][(rg + 16 * i) * LDK + pl] = ra[i];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) Bs[buf][(rg + 16 * i) * LDK + pl] = rb[i];
+  };
+
+  v4f acc[TM][TN];
+#pragma unroll
+  for (int x = 0; x < TM; ++x)
+#pragma unroll
+    for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+  const int wm0 = (wave % WM) * TM * 16, wn0 = (wave / WM) * TN * 16;
+  const int T = (L1 - L0 + BK - 1) / BK;
+  load();
+  store(0);
+  __syncthreads();
+  for (int t = 0; t < T; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < T) {
+      advance();
+      load();
+    }
+    mma_stage<TM, TN>(As[cur], Bs[cur], wm0, wn0, lane, acc);
+    if (t + 1 < T) store(cur ^ 1);
+    __syncthreads();
+  }
+
+  float* out = a.splits == 1 ? a.dw + (int64_t)j * a.pstride
+                             : a.partial + (int64_t)(j * a.splits + split) * Mo * No;
+#pragma unroll
+  for (int x = 0; x < TM; ++x)
+#pragma unroll
+    for (int y = 0; y < TN; ++y) {
+      const int n = n0 + wn0 + y * 16 + (lane & 15);
+      const int mb = m0 + wm0 + x * 16 + (lane >> 4) * 4;
+      if (n >= No) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (mb + i < Mo) out[(int64_t)(mb + i) * No + n] = acc[x][y][i];
+    }
+}
+
+__global__ __launch_bounds__(256) void reduce_splits_k(const float* part, int splits, int64_t n,
+                                                       float* dw, int64_t pstride) {
+  const int j = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= n) return;
+  const float* p = part + (int64_t)j * splits * n + e;
+  float s = 0.f;
+  for (int i = 0; i < splits; ++i) s += p[(int64_t)i * n];
+  dw[(int64_t)j * pstride + e] = s;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// db[j][c]: one block per (c, j), fixed-order reduction.
+__global__ __launch_bounds__(256) void channel_sum_k(const float* dy, int b, int C, int HW,
+                                                     float* db, int64_t pstride) {
+  __shared__ float red[4];
+  const int c = blockIdx.x, j = blockIdx.y;
+  const int n = b * HW;
+  float s = 0.f;
+  for (int e = threadIdx.x; e < n; e += 256) {
+    const int img = e / HW, p = e - img * HW;
+    s += dy[((int64_t)(j * b + img) * C + c) * HW + p];
+  }
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) db[(int64_t)j * pstride + c] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+
+// Name of one kernel instantiation, as the profiler shows its template.
+template <int KIND, int BM, int BN, int WM, int WN, int R, int ST = 0>
+const char* tile_name() {
+  static const char* base[3] = {"conv_fwd_k", "conv_bwd_data_k", "conv_bwd_weight_k"};
+  static const std::string n = std::string(base[KIND]) + "<" + std::to_string(BM) + ", " +
+                               std::to_string(BN) + ", " + std::to_string(WM) + ", " +
+                               std::to_string(WN) + ", " + std::to_string(R) +
+                               (ST ? ", " + std::to_string(ST) : "") + ">";
+  return n.c_str();
+}
+
+template <int BM, int BN, int WM, int WN, int R>
+hipError_t launch_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
+  const int M = a.g.b * a.g.Ho * a.g.Wo;
+  dim3 grid(cdiv(M, BM), cdiv(a.g.Co, BN), a.g.k);
+  hipLaunchKernelGGL((conv_fwd_k<BM, BN, WM, WN, R>), grid, dim3(256), 0, s, a);
+  if (name) *name = tile_name<0, BM, BN, WM, WN, R>();
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int R, int ST>
+hipError_t launch_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
+  const int M = a.g.b * a.g.H * a.g.W;
+  dim3 grid(cdiv(M, BM), cdiv(a.g.Ci, BN), a.g.k);
+  hipLaunchKernelGGL((conv_bwd_data_k<BM, BN, WM, WN, R, ST>), grid, dim3(256), 0, s, a);
+  if (name) *name = tile_name<1, BM, BN, WM, WN, R, ST>();
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int R>
+hipError_t launch_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char** name) {
+  dim3 grid(cdiv(a.g.Co, BM), cdiv(a.g.Ci * R * R, BN), a.g.k * a.splits);
+  hipLaunchKernelGGL((conv_bwd_weight_k<BM, BN, WM, WN, R>), grid, dim3(256), 0, s, a);
+  if (name) *name = tile_name<2, BM, BN, WM, WN, R>();
+  return hipGetLastError();
+}
+
+int bwd_weight_bm(int Co) { return Co <= 16 ? 16 : (Co <= 32 ? 32 : 64); }
+
+// Enough workgroups to give every CU at least two.
+constexpr int64_t MIN_WGS = 512;
+
+// Output-tile choice for the forward / data-gradient GEMM (M x N per
+// replica): the biggest tile of the N class that still yields MIN_WGS
+// workgroups over all replicas, else the smallest.  Returns 0..5:
+//   0 (256,16)  1 (64,16)  2 (128,32)  3 (64,32)  4 (128,64)  5 (64,64)
+int pick_tile(int64_t M, int N, int k) {
+  auto wgs = [&](int bm, int bn) { return (int64_t)cdiv(M, bm) * cdiv(N, bn) * k; };
+  if (N <= 16) return wgs(256, 16) >= MIN_WGS ? 0 : 1;
+  if (N <= 32) return wgs(128, 32) >= MIN_WGS ? 2 : 3;
+  return wgs(128, 64) >= MIN_WGS ? 4 : 5;
+}
+
+template <int R>
+hipError_t fwd_r(const ConvFwdArgs& a, hipStream_t s, const char** name) {
+  switch (pick_tile((int64_t)a.g.b * a.g.Ho * a.g.Wo, a.g.Co, a.g.k)) {
+    case 0: return launch_fwd<256, 16, 4, 1, R>(a, s, name);
+    case 1: return launch_fwd<64, 16, 4, 1, R>(a, s, name);
+    case 2: return launch_fwd<128, 32, 4, 1, R>(a, s, name);
+    case 3: return launch_fwd<64, 32, 4, 1, R>(a, s, name);
+    case 4: return launch_fwd<128, 64, 2, 2, R>(a, s, name);
+    default: return launch_fwd<64, 64, 2, 2, R>(a, s, name);
+  }
+}
+
+template <int R, int ST>
+hipError_t bwd_data_r(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
+  switch (pick_tile((int64_t)a.g.b * a.g.H * a.g.W, a.g.Ci, a.g.k)) {
+    case 0: return launch_bwd_data<256, 16, 4, 1, R, ST>(a, s, name);
+    case 1: return launch_bwd_data<64, 16, 4, 1, R, ST>(a, s, name);
+    case 2: return launch_bwd_data<128, 32, 4, 1, R, ST>(a, s, name);
+    case 3: return launch_bwd_data<64, 32, 4, 1, R, ST>(a, s, name);
+    case 4: return launch_bwd_data<128, 64, 2, 2, R, ST>(a, s, name);
+    default: return launch_bwd_data<64, 64, 2, 2, R, ST>(a, s, name);
+  }
+}
+
+template <int R>
+hipError_t bwd_weight_r(const ConvBwdWeightArgs& a, hipStream_t s, const char** name) {
+  switch (bwd_weight_bm(a.g.Co)) {
+    case 16: return launch_bwd_weight<16, 64, 1, 4, R>(a, s, name);
+    case 32: return launch_bwd_weight<32, 64, 2, 2, R>(a, s, name);
+    default: return launch_bwd_weight<64, 64, 2, 2, R>(a, s, name);
+  }
+}
+
+}  // namespace
+
+int conv_bwd_weight_splits(const ConvGeom& g, int* chunk) {
+  const int L = g.b * g.Ho * g.Wo;
+  const int bm = bwd_weight_bm(g.Co);
+  const int64_t tiles = (int64_t)cdiv(g.Co, bm) * cdiv(g.Ci * g.R * g.S, 64) * g.k;
+  int splits = (int)std::max<int64_t>(1, std::min<int64_t>(cdiv(L, 64), cdiv(1024, tiles)));
+  int c = (int)cdiv(L, splits);
+  c = (c + BK - 1) / BK * BK;
+  *chunk = c;
+  return (int)cdiv(L, c);
+}
+
+bool conv_supported(int R, int S, int st, bool need_dx) {
+  if (R != S || st < 1 || st > 2) return false;
+  if (R == 1 || R == 3) return true;
+  if (R == 5) return !need_dx || st == 1;
+  if (R == 7) return !need_dx;
+  return false;
+}
+
+hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
+  switch (a.g.R) {
+    case 1: return fwd_r<1>(a, s, name);
+    case 3: return fwd_r<3>(a, s, name);
+    case 5: return fwd_r<5>(a, s, name);
+    case 7: return fwd_r<7>(a, s, name);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
+  const int key = a.g.R * 10 + a.g.st;
+  switch (key) {
+    case 11: return bwd_data_r<1, 1>(a, s, name);
+    case 12: return bwd_data_r<1, 2>(a, s, name);
+    case 31: return bwd_data_r<3, 1>(a, s, name);
+    case 32: return bwd_data_r<3, 2>(a, s, name);
+    case 51: return bwd_data_r<5, 1>(a, s, name);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char** name) {
+  switch (a.g.R) {
+    case 1: return bwd_weight_r<1>(a, s, name);
+    case 3: return bwd_weight_r<3>(a, s, name);
+    case 5: return bwd_weight_r<5>(a, s, name);
+    case 7: return bwd_weight_r<7>(a, s, name);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t reduce_splits(const float* partial, int k, int splits, int64_t n, float* dw,
+                         int64_t pstride, hipStream_t s) {
+  hipLaunchKernelGGL(reduce_splits_k, dim3(cdiv(n, 256), k), dim3(256), 0, s, partial, splits, n,
+                     dw, pstride);
+  return hipGetLastError();
+}
+
+hipError_t channel_sum(const float* dy, int k, int b, int C, int HW, float* db, int64_t pstride,
+                       hipStream_t s) {
+  hipLaunchKernelGGL(channel_sum_k, dim3(C, k), dim3(256), 0, s, dy, b, C, HW, db, pstride);
+  return hipGetLastError();
+}
+
+}  // namespace cbk

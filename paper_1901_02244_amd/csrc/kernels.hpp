@@ -1,0 +1,154 @@
+// kernels.hpp -- launch interface of the HIP kernels (gfx950).
+//
+// All activations are fp32 NCHW over the k*b images of one iteration;
+// replica j owns images [j*b, (j+1)*b).  Parameters of replica j start at
+// params + j*pstride.  Every launcher enqueues on the given stream and
+// returns the hipError_t of the launch.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cbk {
+
+// Geometry of one convolution layer (an FC layer is a 1x1 conv on a 1x1
+// image).  b = images per replica, k = replicas.
+struct ConvGeom {
+  int k, b;
+  int Ci, H, W;
+  int Co, R, S;
+  int st, pad;
+  int Ho, Wo;
+};
+
+struct ConvFwdArgs {
+  ConvGeom g;
+  const float* x;     // [k*b][Ci][H][W]
+  const float* w;     // replica 0 weights [Co][Ci][R][S]
+  const float* bias;  // replica 0 bias [Co] or nullptr
+  int64_t pstride;    // elements between replicas' parameters
+  float* y;           // [k*b][Co][Ho][Wo]
+  int relu;
+};
+
+// Residual added to a data gradient (the shortcut of a residual block):
+//   ADD_SAME: add src at the same index;
+//   ADD_SUBSAMPLE: src is [k*b][Csrc][H/st][W/st]; dX[n][c][h][w] gets
+//     src[n][c][h/st][w/st] when h and w are multiples of st (option-A
+//     shortcut read backwards; c < Ci <= Csrc).
+enum { ADD_NONE = 0, ADD_SAME = 1, ADD_SUBSAMPLE = 2 };
+
+struct ConvBwdDataArgs {
+  ConvGeom g;
+  const float* dy;    // [k*b][Co][Ho][Wo]
+  const float* w;     // replica 0 weights
+  int64_t pstride;
+  float* dx;          // [k*b][Ci][H][W]
+  int accumulate;     // dx += result instead of dx = result
+  const float* mask;  // zero dx where mask <= 0 (a fused ReLU upstream), or nullptr
+  const float* add;   // residual gradient, or nullptr
+  int add_mode, add_C, add_st;
+};
+
+struct ConvBwdWeightArgs {
+  ConvGeom g;
+  const float* x;     // [k*b][Ci][H][W]
+  const float* dy;    // [k*b][Co][Ho][Wo]
+  float* dw;          // replica 0 gradient [Co][Ci][R][S] (splits == 1)
+  int64_t pstride;
+  float* partial;     // [k][splits][Co][Ci*R*S] (splits > 1)
+  int splits, chunk;  // contraction (b*Ho*Wo) split into `splits` chunks
+};
+
+// Square filters R in {1, 3, 5, 7}, stride 1 or 2; the data gradient is
+// built for (R, stride) in {(1,1), (1,2), (3,1), (3,2), (5,1)}.
+bool conv_supported(int R, int S, int st, bool need_dx);
+// Split of the weight-gradient contraction; exposed so the host can size scratch.
+int conv_bwd_weight_splits(const ConvGeom& g, int* chunk);
+
+// The conv launchers pick a tile shape from the layer's sizes; *name (if
+// not null) receives the launched kernel's name, for instrumentation.
+hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name = nullptr);
+hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name = nullptr);
+hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s,
+                           const char** name = nullptr);
+// dw[j][e] = sum over splits of partial[j][s][e], s in order.
+hipError_t reduce_splits(const float* partial, int k, int splits, int64_t n, float* dw,
+                         int64_t pstride, hipStream_t s);
+// db[j][c] = sum over replica j's images and pixels of dy[n][c][p].
+hipError_t channel_sum(const float* dy, int k, int b, int C, int HW, float* db,
+                       int64_t pstride, hipStream_t s);
+
+// Batch norm with per-replica batch statistics.
+enum { RES_NONE = 0, RES_SAME = 1, RES_SUBSAMPLE = 2 };
+
+struct BNArgs {
+  int k, b, C, H, W;
+  const float* x;       // conv output [k*b][C][H][W]
+  float* y;             // output
+  const float* gamma;   // replica 0 gamma [C]; beta follows at gamma + C
+  int64_t pstride;
+  float* mean;          // [k][C] saved for backward
+  float* istd;          // [k][C]
+  double* part;         // scratch [k][C][chunks][2]
+  int chunks;
+  int relu;
+  const float* res;     // residual input or nullptr
+  int res_mode, res_C, res_st, res_H, res_W;
+};
+
+struct BNBwdArgs {
+  int k, b, C, H, W;
+  const float* x;       // conv output (BN input)
+  const float* y;       // BN output (for the ReLU mask) or nullptr
+  const float* dy;      // gradient at the BN output (before the ReLU mask)
+  float* dx;            // gradient at the BN input
+  float* dres;          // masked output gradient for the shortcut, or nullptr
+  const float* gamma;
+  float* dgamma;        // replica 0 gradient of gamma; beta's follows at + C
+  int64_t pstride;
+  const float* mean;
+  const float* istd;
+  double* part;
+  int chunks;
+};
+
+int bn_chunks(int b, int HW, int C, int k);
+// Forward: per-chunk fp64 sums, then normalise (+ residual, ReLU).
+hipError_t bn_fwd_stats(const BNArgs& a, hipStream_t s);
+hipError_t bn_fwd_apply(const BNArgs& a, hipStream_t s);
+// Backward: per-chunk fp64 sums of dy and dy*xhat, then dx (and dgamma/dbeta).
+hipError_t bn_bwd_stats(const BNBwdArgs& a, hipStream_t s);
+hipError_t bn_bwd_apply(const BNBwdArgs& a, hipStream_t s);
+
+hipError_t maxpool_fwd(const float* x, int N, int C, int H, int W, int K, int st, int pad,
+                       float* y, int Ho, int Wo, int* arg, hipStream_t s);
+// dx over the whole input; mask_relu zeroes entries whose input was <= 0.
+hipError_t maxpool_bwd(const float* dy, const int* arg, const float* x, int N, int C, int H,
+                       int W, int K, int st, int pad, int Ho, int Wo, float* dx, int mask_relu,
+                       hipStream_t s);
+hipError_t gap_fwd(const float* x, int N, int C, int HW, float* y, hipStream_t s);
+hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t s);
+// Mean softmax cross-entropy per replica and its gradient wrt the logits.
+hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b, int classes,
+                        float* dlogits, float* loss, hipStream_t s);
+
+// Fused SMA synchronisation (Algorithm 1).  W, G, Wprev are [k][stride];
+// z, zp are [>= P] with P padded to a multiple of 4 elements.
+struct SMAArgs {
+  float* W;
+  const float* G;
+  float* Wprev;          // nullptr unless learner momentum is on
+  float* z;
+  float* zp;
+  int k;
+  int64_t P4;            // number of float4 columns
+  int64_t wstride4, gstride4;
+  float alpha, lr, mu, mu_l;
+  int correct;           // 0: local step only (no correction, z untouched)
+};
+hipError_t sma_step(const SMAArgs& a, hipStream_t s);
+// flag[0] = 1 if any of z[0..n) is NaN/Inf (flag must be zeroed first).
+hipError_t nonfinite_scan(const float* z, int64_t n, int* flag, hipStream_t s);
+hipError_t zero_ints(int* p, int n, hipStream_t s);
+
+}  // namespace cbk

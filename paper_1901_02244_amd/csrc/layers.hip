@@ -1,0 +1,353 @@
+// layers.hip -- the memory-bound layers of a learner's forward and backward
+// pass (Sec. 2.1), batched over all k learners of the GPU.
+//
+// Batch norm uses each learner's own batch statistics (learners are
+// independent, Sec. 3.1).  Every reduction runs in a fixed order (per-thread
+// partial, wave butterfly, then the four waves in order; partials across
+// blocks are combined in block order), so results are bitwise reproducible.
+// Statistics are accumulated in fp64.
+#include "kernels.hpp"
+
+#include <algorithm>
+
+namespace cbk {
+namespace {
+
+constexpr double BN_EPS = 1e-5;
+
+inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_sum_f(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max_f(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Sum of two doubles over a 256-thread block, fixed order; result in all threads.
+__device__ __forceinline__ void block_sum2(double& a, double& b, double* red) {
+  a = wave_sum_d(a);
+  b = wave_sum_d(b);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    red[w] = a;
+    red[4 + w] = b;
+  }
+  __syncthreads();
+  a = (red[0] + red[1]) + (red[2] + red[3]);
+  b = (red[4] + red[5]) + (red[6] + red[7]);
+}
+
+// The elements of (replica j, channel c) are e in [0, b*HW): image e / HW of
+// the replica, pixel e % HW.  Block `chunk` owns e in [e0, e1).
+struct ChanIter {
+  int img, p;
+  __device__ ChanIter(int e, int HW) : img(e / HW), p(e - (e / HW) * HW) {}
+  __device__ void step(int d, int HW) {
+    p += d;
+    while (p >= HW) {
+      p -= HW;
+      ++img;
+    }
+  }
+};
+
+__global__ __launch_bounds__(256) void bn_stats_k(BNArgs a) {
+  __shared__ double red[8];
+  const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
+  const int HW = a.H * a.W, n = a.b * HW;
+  const int per = (n + a.chunks - 1) / a.chunks;
+  const int e0 = chunk * per, e1 = min(n, e0 + per);
+  double s = 0.0, ss = 0.0;
+  const float* X = a.x + ((int64_t)j * a.b * a.C + c) * HW;
+  ChanIter it(e0 + threadIdx.x, HW);
+  for (int e = e0 + threadIdx.x; e < e1; e += 256, it.step(256, HW)) {
+    const double v = X[(int64_t)it.img * a.C * HW + it.p];
+    s += v;
+    ss += v * v;
+  }
+  block_sum2(s, ss, red);
+  if (threadIdx.x == 0) {
+    double* p = a.part + (((int64_t)j * a.C + c) * a.chunks + chunk) * 2;
+    p[0] = s;
+    p[1] = ss;
+  }
+}
+
+__global__ __launch_bounds__(256) void bn_apply_k(BNArgs a) {
+  const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
+  const int HW = a.H * a.W, n = a.b * HW;
+  const int per = (n + a.chunks - 1) / a.chunks;
+  const int e0 = chunk * per, e1 = min(n, e0 + per);
+  const double* p = a.part + ((int64_t)j * a.C + c) * a.chunks * 2;
+  double s = 0.0, ss = 0.0;
+  for (int i = 0; i < a.chunks; ++i) {
+    s += p[2 * i];
+    ss += p[2 * i + 1];
+  }
+  const double mean = s / n;
+  const double var = fmax(ss / n - mean * mean, 0.0);
+  const float mf = (float)mean, isf = (float)(1.0 / sqrt(var + BN_EPS));
+  if (chunk == 0 && threadIdx.x == 0) {
+    a.mean[j * a.C + c] = mf;
+    a.istd[j * a.C + c] = isf;
+  }
+  const float* gam = a.gamma + (int64_t)j * a.pstride;
+  const float ga = gam[c], be = gam[a.C + c];
+  const int64_t base = ((int64_t)j * a.b * a.C + c) * HW;
+  const float* X = a.x + base;
+  float* Y = a.y + base;
+  ChanIter it(e0 + threadIdx.x, HW);
+  for (int e = e0 + threadIdx.x; e < e1; e += 256, it.step(256, HW)) {
+    const int64_t off = (int64_t)it.img * a.C * HW + it.p;
+    float v = ga * ((X[off] - mf) * isf) + be;
+    if (a.res_mode == RES_SAME) {
+      v += a.res[base + off];
+    } else if (a.res_mode == RES_SUBSAMPLE) {
+      if (c < a.res_C) {
+        const int oh = it.p / a.W, ow = it.p - oh * a.W;
+        const int img = j * a.b + it.img;
+        v += a.res[(((int64_t)img * a.res_C + c) * a.res_H + oh * a.res_st) * a.res_W +
+                   ow * a.res_st];
+      }
+    }
+    if (a.relu) v = v > 0.f ? v : 0.f;
+    Y[off] = v;
+  }
+}
+
+__global__ __launch_bounds__(256) void bn_bwd_stats_k(BNBwdArgs a) {
+  __shared__ double red[8];
+  const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
+  const int HW = a.H * a.W, n = a.b * HW;
+  const int per = (n + a.chunks - 1) / a.chunks;
+  const int e0 = chunk * per, e1 = min(n, e0 + per);
+  const float mf = a.mean[j * a.C + c], isf = a.istd[j * a.C + c];
+  const int64_t base = ((int64_t)j * a.b * a.C + c) * HW;
+  double s = 0.0, sx = 0.0;
+  ChanIter it(e0 + threadIdx.x, HW);
+  for (int e = e0 + threadIdx.x; e < e1; e += 256, it.step(256, HW)) {
+    const int64_t off = base + (int64_t)it.img * a.C * HW + it.p;
+    float d = a.dy[off];
+    if (a.y && !(a.y[off] > 0.f)) d = 0.f;
+    const float xh = (a.x[off] - mf) * isf;
+    s += d;
+    sx += (double)d * xh;
+  }
+  block_sum2(s, sx, red);
+  if (threadIdx.x == 0) {
+    double* p = a.part + (((int64_t)j * a.C + c) * a.chunks + chunk) * 2;
+    p[0] = s;
+    p[1] = sx;
+  }
+}
+
+__global__ __launch_bounds__(256) void bn_bwd_apply_k(BNBwdArgs a) {
+  const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
+  const int HW = a.H * a.W, n = a.b * HW;
+  const int per = (n + a.chunks - 1) / a.chunks;
+  const int e0 = chunk * per, e1 = min(n, e0 + per);
+  const double* p = a.part + ((int64_t)j * a.C + c) * a.chunks * 2;
+  double s = 0.0, sx = 0.0;
+  for (int i = 0; i < a.chunks; ++i) {
+    s += p[2 * i];
+    sx += p[2 * i + 1];
+  }
+  const float mf = a.mean[j * a.C + c], isf = a.istd[j * a.C + c];
+  const float ga = a.gamma[(int64_t)j * a.pstride + c];
+  if (chunk == 0 && threadIdx.x == 0) {
+    a.dgamma[(int64_t)j * a.pstride + c] = (float)sx;
+    a.dgamma[(int64_t)j * a.pstride + a.C + c] = (float)s;
+  }
+  const float k1 = ga * isf, mdy = (float)(s / n), mdyx = (float)(sx / n);
+  const int64_t base = ((int64_t)j * a.b * a.C + c) * HW;
+  ChanIter it(e0 + threadIdx.x, HW);
+  for (int e = e0 + threadIdx.x; e < e1; e += 256, it.step(256, HW)) {
+    const int64_t off = base + (int64_t)it.img * a.C * HW + it.p;
+    float d = a.dy[off];
+    if (a.y && !(a.y[off] > 0.f)) d = 0.f;
+    const float xh = (a.x[off] - mf) * isf;
+    a.dx[off] = k1 * (d - mdy - xh * mdyx);
+    if (a.dres) a.dres[off] = d;
+  }
+}
+
+// Max pool: the first cell (row-major) whose value is strictly greater than
+// all earlier ones wins; padded cells never win.
+__global__ __launch_bounds__(256) void maxpool_fwd_k(const float* x, int NC, int H, int W, int K,
+                                                     int st, int pad, float* y, int Ho, int Wo,
+                                                     int* arg) {
+  const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (o >= (int64_t)NC * Ho * Wo) return;
+  const int ow = (int)(o % Wo), oh = (int)((o / Wo) % Ho);
+  const int64_t nc = o / ((int64_t)Ho * Wo);
+  const float* xp = x + nc * H * W;
+  int best = -1;
+  float bv = 0.f;
+  for (int r = 0; r < K; ++r) {
+    const int ih = oh * st - pad + r;
+    if (ih < 0 || ih >= H) continue;
+    for (int s = 0; s < K; ++s) {
+      const int iw = ow * st - pad + s;
+      if (iw < 0 || iw >= W) continue;
+      const float v = xp[ih * W + iw];
+      if (best < 0 || v > bv) {
+        best = ih * W + iw;
+        bv = v;
+      }
+    }
+  }
+  y[o] = bv;
+  arg[o] = best;
+}
+
+// Gradient of max pool, gathered per input cell over the windows that can
+// contain it (no atomics): windows visited in row-major order.
+__global__ __launch_bounds__(256) void maxpool_bwd_k(const float* dy, const int* arg,
+                                                     const float* x, int NC, int H, int W, int K,
+                                                     int st, int pad, int Ho, int Wo, float* dx,
+                                                     int mask_relu) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)NC * H * W) return;
+  const int iw = (int)(i % W), ih = (int)((i / W) % H);
+  const int64_t nc = i / ((int64_t)H * W);
+  const int cell = ih * W + iw;
+  // windows oh with oh*st - pad <= ih <= oh*st - pad + K - 1
+  const int oh_lo = max(0, (ih + pad - K + st) / st), oh_hi = min(Ho - 1, (ih + pad) / st);
+  const int ow_lo = max(0, (iw + pad - K + st) / st), ow_hi = min(Wo - 1, (iw + pad) / st);
+  float s = 0.f;
+  for (int oh = oh_lo; oh <= oh_hi; ++oh)
+    for (int ow = ow_lo; ow <= ow_hi; ++ow) {
+      const int64_t o = (nc * Ho + oh) * Wo + ow;
+      if (arg[o] == cell) s += dy[o];
+    }
+  if (mask_relu && !(x[i] > 0.f)) s = 0.f;
+  dx[i] = s;
+}
+
+__global__ __launch_bounds__(256) void gap_fwd_k(const float* x, int64_t NC, int HW, float* y) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= NC) return;
+  const float* p = x + i * HW;
+  float s = 0.f;
+  for (int e = 0; e < HW; ++e) s += p[e];
+  y[i] = s / HW;
+}
+
+__global__ __launch_bounds__(256) void gap_bwd_k(const float* dy, int64_t n, int HW, float* dx) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  dx[i] = dy[i / HW] / HW;
+}
+
+// One block per learner: mean over its b images of -log softmax(o)_y and
+// the gradient (softmax(o) - onehot(y)) / b (Eq. 2).
+__global__ __launch_bounds__(256) void softmax_xent_k(const float* logits, const int32_t* labels,
+                                                      int b, int classes, float* dlogits,
+                                                      float* loss) {
+  __shared__ float red[4];
+  const int j = blockIdx.x, t = threadIdx.x, w = t >> 6;
+  double tot = 0.0;
+  for (int i = 0; i < b; ++i) {
+    const int64_t row = (int64_t)(j * b + i) * classes;
+    const float* o = logits + row;
+    float mx = -INFINITY;
+    for (int c = t; c < classes; c += 256) mx = fmaxf(mx, o[c]);
+    mx = wave_max_f(mx);
+    __syncthreads();
+    if ((t & 63) == 0) red[w] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    float se = 0.f;
+    for (int c = t; c < classes; c += 256) se += expf(o[c] - mx);
+    se = wave_sum_f(se);
+    __syncthreads();
+    if ((t & 63) == 0) red[w] = se;
+    __syncthreads();
+    se = (red[0] + red[1]) + (red[2] + red[3]);
+    const float lse = mx + logf(se);
+    const int y = labels[j * b + i];
+    const bool yok = (unsigned)y < (unsigned)classes;
+    for (int c = t; c < classes; c += 256)
+      dlogits[row + c] = (expf(o[c] - lse) - (c == y ? 1.f : 0.f)) / b;
+    if (t == 0) tot += yok ? (double)(lse - o[y]) : (double)NAN;
+  }
+  if (t == 0) loss[j] = (float)(tot / b);
+}
+
+}  // namespace
+
+int bn_chunks(int b, int HW, int C, int k) {
+  const int n = b * HW;
+  int chunks = (int)cdiv(512, (int64_t)C * k);
+  chunks = std::min(chunks, (int)cdiv(n, 1024));
+  return std::max(1, chunks);
+}
+
+hipError_t bn_fwd_stats(const BNArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(bn_stats_k, dim3(a.chunks, a.C, a.k), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t bn_fwd_apply(const BNArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(bn_apply_k, dim3(a.chunks, a.C, a.k), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t bn_bwd_stats(const BNBwdArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(bn_bwd_stats_k, dim3(a.chunks, a.C, a.k), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t bn_bwd_apply(const BNBwdArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(bn_bwd_apply_k, dim3(a.chunks, a.C, a.k), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t maxpool_fwd(const float* x, int N, int C, int H, int W, int K, int st, int pad,
+                       float* y, int Ho, int Wo, int* arg, hipStream_t s) {
+  const int64_t n = (int64_t)N * C * Ho * Wo;
+  hipLaunchKernelGGL(maxpool_fwd_k, dim3(cdiv(n, 256)), dim3(256), 0, s, x, N * C, H, W, K, st,
+                     pad, y, Ho, Wo, arg);
+  return hipGetLastError();
+}
+
+hipError_t maxpool_bwd(const float* dy, const int* arg, const float* x, int N, int C, int H,
+                       int W, int K, int st, int pad, int Ho, int Wo, float* dx, int mask_relu,
+                       hipStream_t s) {
+  const int64_t n = (int64_t)N * C * H * W;
+  hipLaunchKernelGGL(maxpool_bwd_k, dim3(cdiv(n, 256)), dim3(256), 0, s, dy, arg, x, N * C, H, W,
+                     K, st, pad, Ho, Wo, dx, mask_relu);
+  return hipGetLastError();
+}
+
+hipError_t gap_fwd(const float* x, int N, int C, int HW, float* y, hipStream_t s) {
+  const int64_t nc = (int64_t)N * C;
+  hipLaunchKernelGGL(gap_fwd_k, dim3(cdiv(nc, 256)), dim3(256), 0, s, x, nc, HW, y);
+  return hipGetLastError();
+}
+
+hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t s) {
+  const int64_t n = (int64_t)N * C * HW;
+  hipLaunchKernelGGL(gap_bwd_k, dim3(cdiv(n, 256)), dim3(256), 0, s, dy, n, HW, dx);
+  return hipGetLastError();
+}
+
+hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b, int classes,
+                        float* dlogits, float* loss, hipStream_t s) {
+  hipLaunchKernelGGL(softmax_xent_k, dim3(k), dim3(256), 0, s, logits, labels, b, classes,
+                     dlogits, loss);
+  return hipGetLastError();
+}
+
+}  // namespace cbk

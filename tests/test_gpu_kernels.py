@@ -1,0 +1,269 @@
+"""Kernel-level parity through the operator test hooks of the C ABI (GPU).
+
+Each operator of the learning task runs through the same launchers as
+cb_step (same kernels, same tile choices) at the exact layer shapes of the
+three workloads -- LeNet k=8 b=16, ResNet-32 k=4 b=32, ResNet-50 k=2 b=32
+-- and at ragged shapes that leave partial tiles.  Both sides get the same
+fp32 inputs, so no ReLU or max-pool decision can differ and the method's
+one-step bar (per-tensor max relative error <= 1e-4) applies to every
+output.  Small layers are compared whole; for large ones the oracle
+computes sampled elements one by one from the definition.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1901_02244_amd as cb
+from parity import TOL_STEP1, max_rel
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+# (name, k, b, Ci, H, Co, R, stride, pad, relu, bias, need_dx)
+CONV = [
+    # LeNet-5, 8 learners of 16 images
+    ("lenet.conv1", 8, 16, 1, 28, 6, 5, 1, 2, 1, 1, 0),
+    ("lenet.conv2", 8, 16, 6, 14, 16, 5, 1, 0, 1, 1, 1),
+    ("lenet.fc1", 8, 16, 400, 1, 120, 1, 1, 0, 1, 1, 1),
+    ("lenet.fc2", 8, 16, 120, 1, 84, 1, 1, 0, 1, 1, 1),
+    ("lenet.fc3", 8, 16, 84, 1, 10, 1, 1, 0, 0, 1, 1),
+    # ResNet-32, 4 learners of 32 images
+    ("r32.stem", 4, 32, 3, 32, 16, 3, 1, 1, 0, 0, 0),
+    ("r32.s1", 4, 32, 16, 32, 16, 3, 1, 1, 0, 0, 1),
+    ("r32.s2.down", 4, 32, 16, 32, 32, 3, 2, 1, 0, 0, 1),
+    ("r32.s2", 4, 32, 32, 16, 32, 3, 1, 1, 0, 0, 1),
+    ("r32.s3.down", 4, 32, 32, 16, 64, 3, 2, 1, 0, 0, 1),
+    ("r32.s3", 4, 32, 64, 8, 64, 3, 1, 1, 0, 0, 1),
+    ("r32.fc", 4, 32, 64, 1, 10, 1, 1, 0, 0, 1, 1),
+    # ResNet-50, 2 learners of 32 images (224 x 224)
+    ("r50.stem", 2, 32, 3, 224, 64, 7, 2, 3, 0, 0, 0),
+    ("r50.s1.a", 2, 32, 64, 56, 64, 1, 1, 0, 0, 0, 1),
+    ("r50.s1.b", 2, 32, 64, 56, 64, 3, 1, 1, 0, 0, 1),
+    ("r50.s1.c", 2, 32, 64, 56, 256, 1, 1, 0, 0, 0, 1),
+    ("r50.s1.a2", 2, 32, 256, 56, 64, 1, 1, 0, 0, 0, 1),
+    ("r50.s2.a", 2, 32, 256, 56, 128, 1, 2, 0, 0, 0, 1),
+    ("r50.s2.proj", 2, 32, 256, 56, 512, 1, 2, 0, 0, 0, 1),
+    ("r50.s2.b", 2, 32, 128, 28, 128, 3, 1, 1, 0, 0, 1),
+    ("r50.s3.b", 2, 32, 256, 14, 256, 3, 1, 1, 0, 0, 1),
+    ("r50.s3.c", 2, 32, 256, 14, 1024, 1, 1, 0, 0, 0, 1),
+    ("r50.s4.a", 2, 32, 1024, 14, 512, 1, 2, 0, 0, 0, 1),
+    ("r50.s4.b", 2, 32, 512, 7, 512, 3, 1, 1, 0, 0, 1),
+    ("r50.s4.a2", 2, 32, 2048, 7, 512, 1, 1, 0, 0, 0, 1),
+    ("r50.fc", 2, 32, 2048, 1, 1000, 1, 1, 0, 0, 1, 1),
+    # ragged: partial tiles in every GEMM dimension
+    ("ragged.3x3s2", 3, 5, 7, 13, 19, 3, 2, 1, 0, 0, 1),
+    ("ragged.5x5", 2, 3, 5, 11, 37, 5, 1, 2, 1, 1, 1),
+    ("ragged.1x1s2", 3, 2, 70, 9, 45, 1, 2, 0, 0, 0, 1),
+    ("ragged.fc", 5, 3, 33, 1, 17, 1, 1, 0, 1, 1, 1),
+    ("ragged.7x7s2", 2, 3, 3, 19, 5, 7, 2, 3, 0, 0, 0),
+]
+
+FULL_LIMIT = 6e8  # multiply-adds per replica below which the oracle does whole tensors
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _rng(tag):
+    return np.random.default_rng(zlib.crc32(tag.encode()))
+
+
+def _sample_idx(rng, shape, n):
+    return np.stack([rng.integers(0, d, n) for d in shape], axis=1).astype(np.int32)
+
+
+@pytest.mark.parametrize("case", CONV, ids=[c[0] for c in CONV])
+def test_conv_kernels(case):
+    name, k, b, Ci, H, Co, R, st, pad, relu, bias, need_dx = case
+    W = H
+    Ho = (H + 2 * pad - R) // st + 1
+    rng = _rng("conv" + name)
+    nw = Co * Ci * R * R
+    pstride = nw + (Co if bias else 0) + 3  # an odd stride between replicas
+    x = rng.standard_normal((k * b, Ci, H, W), dtype=np.float32)
+    params = np.zeros(k * pstride, dtype=np.float32)
+    for j in range(k):
+        params[j * pstride:j * pstride + nw] = rng.standard_normal(nw) * np.sqrt(2.0 / (Ci * R * R))
+        if bias:
+            params[j * pstride + nw:j * pstride + nw + Co] = rng.standard_normal(Co) * 0.1
+    dy = rng.standard_normal((k * b, Co, Ho, Ho), dtype=np.float32)
+    L = cb.lib()
+    scratch_n = L.cb_test_conv_scratch_bytes(k, b, Ci, H, W, Co, R, st, pad)
+    assert scratch_n > 0
+    xd, pd, dyd = _dev(x), _dev(params), _dev(dy)
+    yd = torch.empty((k * b, Co, Ho, Ho), dtype=torch.float32, device="cuda")
+    dxd = torch.empty_like(xd) if need_dx else None
+    gd = torch.zeros_like(pd)
+    scratch = torch.empty(scratch_n, dtype=torch.uint8, device="cuda")
+    rc = L.cb_test_conv(k, b, Ci, H, W, Co, R, st, pad, relu, bias, xd.data_ptr(), pd.data_ptr(),
+                        pstride, yd.data_ptr(), dyd.data_ptr(),
+                        dxd.data_ptr() if need_dx else None, gd.data_ptr(), scratch.data_ptr(),
+                        scratch_n, torch.cuda.current_stream().cuda_stream)
+    assert rc == 0
+    torch.cuda.synchronize()
+    y, g = yd.cpu().numpy(), gd.cpu().numpy()
+    dx = dxd.cpu().numpy() if need_dx else None
+    macs = b * Ho * Ho * Co * Ci * R * R
+    geo = dict(N=b, Ci=Ci, H=H, W=W, Co=Co, R=R, stride=st, pad=pad)
+    for j in sorted({0, k - 1}):
+        sl = slice(j * b, (j + 1) * b)
+        w = params[j * pstride:j * pstride + nw].reshape(Co, Ci, R, R)
+        bb = params[j * pstride + nw:j * pstride + nw + Co] if bias else None
+        gw = g[j * pstride:j * pstride + nw].reshape(Co, Ci, R, R)
+        if macs <= FULL_LIMIT:
+            yo, dxo, dwo, dbo = oracle.conv2d(x[sl], w, bb, st, pad, dy=dy[sl])
+            if relu:
+                yo = np.maximum(yo, 0.0)
+            assert max_rel(y[sl], yo) <= TOL_STEP1, (name, j, "y")
+            assert max_rel(gw, dwo) <= TOL_STEP1, (name, j, "dw")
+            if bias:
+                assert max_rel(g[j * pstride + nw:j * pstride + nw + Co], dbo) <= TOL_STEP1
+            if need_dx:
+                assert max_rel(dx[sl], dxo) <= TOL_STEP1, (name, j, "dx")
+        else:
+            qy = _sample_idx(rng, (b, Co, Ho, Ho), 512)
+            yo = oracle.conv_samples(0, qy, x=x[sl], w=w, bias=bb, **geo)
+            if relu:
+                yo = np.maximum(yo, 0.0)
+            ys = y[sl][tuple(qy.T)]
+            assert max_rel(ys, yo) <= TOL_STEP1, (name, j, "y")
+            qw = _sample_idx(rng, (Co, Ci, R, R), 256)
+            assert max_rel(gw[tuple(qw.T)], oracle.conv_samples(1, qw, x=x[sl], dy=dy[sl], **geo)) \
+                <= TOL_STEP1, (name, j, "dw")
+            if need_dx:
+                qx = _sample_idx(rng, (b, Ci, H, W), 512)
+                assert max_rel(dx[sl][tuple(qx.T)],
+                               oracle.conv_samples(2, qx, dy=dy[sl], w=w, **geo)) <= TOL_STEP1, \
+                    (name, j, "dx")
+
+
+# (name, k, b, C, H, relu)
+BN = [
+    ("r32.s1", 4, 32, 16, 32, 1),
+    ("r32.s2", 4, 32, 32, 16, 0),
+    ("r32.s3", 4, 32, 64, 8, 1),
+    ("r50.stem", 2, 32, 64, 112, 1),
+    ("r50.s1.c", 2, 32, 256, 56, 0),
+    ("r50.s3", 2, 32, 256, 14, 1),
+    ("r50.s4.c", 2, 32, 2048, 7, 0),
+    ("ragged", 3, 5, 7, 9, 1),
+    ("ragged.1x1", 2, 3, 5, 1, 0),
+]
+
+
+@pytest.mark.parametrize("case", BN, ids=[c[0] for c in BN])
+def test_batchnorm_kernels(case):
+    name, k, b, C, H, relu = case
+    W = H
+    rng = _rng("bn" + name)
+    x = (rng.standard_normal((k * b, C, H, W), dtype=np.float32) * 2 + 0.5).astype(np.float32)
+    dy = rng.standard_normal((k * b, C, H, W), dtype=np.float32)
+    pstride = 2 * C + 1
+    params = np.zeros(k * pstride, dtype=np.float32)
+    for j in range(k):
+        params[j * pstride:j * pstride + C] = 1 + 0.2 * rng.standard_normal(C)
+        params[j * pstride + C:j * pstride + 2 * C] = 0.2 * rng.standard_normal(C)
+    gam = [params[j * pstride:j * pstride + C] for j in range(k)]
+    bet = [params[j * pstride + C:j * pstride + 2 * C] for j in range(k)]
+    yo = np.concatenate([oracle.batchnorm(x[j * b:(j + 1) * b], gam[j], bet[j])[0]
+                         for j in range(k)])
+    dyo = dy
+    if relu:
+        yo = np.maximum(yo, 0.0)
+        # the gradient through the ReLU takes the oracle's decisions on both
+        # sides (the mask is handed to the GPU kernel as an input)
+        dyo = np.where(yo > 0, dy, 0.0)
+    ref = [oracle.batchnorm(x[j * b:(j + 1) * b], gam[j], bet[j], dy=dyo[j * b:(j + 1) * b])
+           for j in range(k)]
+    L = cb.lib()
+    sn = L.cb_test_bn_scratch_bytes(k, b, C, H, W)
+    xd, dyd, pd = _dev(x), _dev(dy), _dev(params)
+    yd = torch.empty_like(xd)
+    mean = torch.empty(k * C, dtype=torch.float32, device="cuda")
+    istd = torch.empty(k * C, dtype=torch.float32, device="cuda")
+    scratch = torch.empty(sn, dtype=torch.uint8, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    assert L.cb_test_bn_fwd(k, b, C, H, W, relu, xd.data_ptr(), pd.data_ptr(), pstride,
+                            yd.data_ptr(), mean.data_ptr(), istd.data_ptr(), scratch.data_ptr(),
+                            sn, st) == 0
+    mask = _dev(yo.astype(np.float32)) if relu else None
+    dxd = torch.empty_like(xd)
+    gd = torch.zeros_like(pd)
+    assert L.cb_test_bn_bwd(k, b, C, H, W, xd.data_ptr(), mask.data_ptr() if relu else None,
+                            dyd.data_ptr(), pd.data_ptr(), pstride, mean.data_ptr(),
+                            istd.data_ptr(), dxd.data_ptr(), gd.data_ptr(), scratch.data_ptr(), sn,
+                            st) == 0
+    torch.cuda.synchronize()
+    assert max_rel(yd.cpu().numpy(), yo) <= TOL_STEP1
+    mu = x.reshape(k, b, C, -1).astype(np.float64).mean(axis=(1, 3))
+    var = x.reshape(k, b, C, -1).astype(np.float64).var(axis=(1, 3))
+    assert max_rel(mean.cpu().numpy(), mu.reshape(-1)) <= TOL_STEP1
+    assert max_rel(istd.cpu().numpy(), (1 / np.sqrt(var + 1e-5)).reshape(-1)) <= TOL_STEP1
+    dx = dxd.cpu().numpy()
+    g = gd.cpu().numpy()
+    for j in range(k):
+        _, dxo, dgo, dbo = ref[j]
+        assert max_rel(dx[j * b:(j + 1) * b], dxo) <= TOL_STEP1, (name, j, "dx")
+        assert max_rel(g[j * pstride:j * pstride + C], dgo) <= TOL_STEP1, (name, j, "dgamma")
+        assert max_rel(g[j * pstride + C:j * pstride + 2 * C], dbo) <= TOL_STEP1, (name, j, "dbeta")
+
+
+# (name, N, C, H, K, stride, pad, mask_relu)
+POOL = [
+    ("lenet.pool1", 128, 6, 28, 2, 2, 0, 1),
+    ("lenet.pool2", 128, 16, 10, 2, 2, 0, 1),
+    ("r50.pool", 64, 64, 112, 3, 2, 1, 0),
+    ("ragged", 3, 5, 11, 3, 2, 1, 1),
+]
+
+
+@pytest.mark.parametrize("case", POOL, ids=[c[0] for c in POOL])
+def test_maxpool_kernels(case):
+    name, N, C, H, K, st, pad, mask = case
+    rng = _rng("pool" + name)
+    x = rng.standard_normal((N, C, H, H), dtype=np.float32)
+    if mask:
+        x = np.maximum(x, 0)  # a ReLU output, with its many zero ties
+    Ho = (H + 2 * pad - K) // st + 1
+    dy = rng.standard_normal((N, C, Ho, Ho), dtype=np.float32)
+    yo, dxo = oracle.maxpool(x, K, st, pad, dy=dy)
+    if mask:
+        dxo = np.where(x > 0, dxo, 0.0)
+    xd, dyd = _dev(x), _dev(dy)
+    yd = torch.empty((N, C, Ho, Ho), dtype=torch.float32, device="cuda")
+    dxd = torch.empty_like(xd)
+    arg = torch.empty((N, C, Ho, Ho), dtype=torch.int32, device="cuda")
+    assert cb.lib().cb_test_maxpool(N, C, H, H, K, st, pad, xd.data_ptr(), yd.data_ptr(),
+                                    dyd.data_ptr(), dxd.data_ptr(), mask, arg.data_ptr(),
+                                    torch.cuda.current_stream().cuda_stream) == 0
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(yd.cpu().numpy(), yo.astype(np.float32))
+    assert max_rel(dxd.cpu().numpy(), dxo) <= 1e-6
+
+
+# (name, k, b, classes)
+XENT = [("lenet", 8, 16, 10), ("r32", 4, 32, 10), ("r50", 2, 32, 1000), ("ragged", 3, 5, 7)]
+
+
+@pytest.mark.parametrize("case", XENT, ids=[c[0] for c in XENT])
+def test_softmax_xent_kernel(case):
+    name, k, b, classes = case
+    rng = _rng("xent" + name)
+    o = (rng.standard_normal((k * b, classes)) * 3).astype(np.float32)
+    y = rng.integers(0, classes, k * b).astype(np.int32)
+    od, yd = _dev(o), _dev(y)
+    dd = torch.empty_like(od)
+    ld = torch.empty(k, dtype=torch.float32, device="cuda")
+    assert cb.lib().cb_test_softmax_xent(k, b, classes, od.data_ptr(), yd.data_ptr(),
+                                         dd.data_ptr(), ld.data_ptr(),
+                                         torch.cuda.current_stream().cuda_stream) == 0
+    torch.cuda.synchronize()
+    d = dd.cpu().numpy()
+    loss = ld.cpu().numpy()
+    for j in range(k):
+        lo, do = oracle.softmax_xent(o[j * b:(j + 1) * b], y[j * b:(j + 1) * b])
+        assert abs(loss[j] - lo) / abs(lo) <= TOL_STEP1
+        assert max_rel(d[j * b:(j + 1) * b], do) <= TOL_STEP1

@@ -12,11 +12,10 @@ import torch.nn.functional as F
 
 import oracle
 
-torch.set_default_dtype(torch.float64)
 
 
 def _t(a, grad=False):
-    return torch.tensor(np.asarray(a, dtype=np.float64), requires_grad=grad)
+    return torch.tensor(np.asarray(a, dtype=np.float64), dtype=torch.float64, requires_grad=grad)
 
 
 CONV_CASES = [
@@ -125,3 +124,26 @@ def test_softmax_xent(oracle_lib):
     # a huge logit gap does not overflow (max-subtracted log-sum-exp)
     l1, _ = oracle.softmax_xent(np.array([[1000.0, 0.0]]), np.array([1]))
     assert abs(l1 - 1000.0) < 1e-9
+
+
+@pytest.mark.parametrize("N,Ci,H,W,Co,R,st,pad,bias", CONV_CASES)
+def test_conv_samples_match_loop_formulation(oracle_lib, N, Ci, H, W, Co, R, st, pad, bias):
+    """Two formulations inside the oracle: whole-tensor loops and one
+    element at a time from the definition."""
+    rng = np.random.default_rng(7 + R)
+    x = rng.standard_normal((N, Ci, H, W)).astype(np.float32)
+    w = rng.standard_normal((Co, Ci, R, R)).astype(np.float32)
+    b = rng.standard_normal(Co).astype(np.float32) if bias else None
+    Ho, Wo = (H + 2 * pad - R) // st + 1, (W + 2 * pad - R) // st + 1
+    dy = rng.standard_normal((N, Co, Ho, Wo)).astype(np.float32)
+    y, dx, dw, db = oracle.conv2d(x, w, b, st, pad, dy=dy)
+    geo = dict(N=N, Ci=Ci, H=H, W=W, Co=Co, R=R, stride=st, pad=pad)
+    qy = np.stack(np.meshgrid(*[np.arange(d) for d in y.shape], indexing="ij"), -1).reshape(-1, 4)
+    np.testing.assert_allclose(oracle.conv_samples(0, qy, x=x, w=w, bias=b, **geo),
+                               y.reshape(-1), rtol=1e-12, atol=1e-12)
+    qw = np.stack(np.meshgrid(*[np.arange(d) for d in w.shape], indexing="ij"), -1).reshape(-1, 4)
+    np.testing.assert_allclose(oracle.conv_samples(1, qw, x=x, dy=dy, **geo), dw.reshape(-1),
+                               rtol=1e-12, atol=1e-11)
+    qx = np.stack(np.meshgrid(*[np.arange(d) for d in x.shape], indexing="ij"), -1).reshape(-1, 4)
+    np.testing.assert_allclose(oracle.conv_samples(2, qx, dy=dy, w=w, **geo), dx.reshape(-1),
+                               rtol=1e-12, atol=1e-11)

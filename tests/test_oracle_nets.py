@@ -19,7 +19,6 @@ import torch.nn.functional as F
 import oracle
 import workloads as wl
 
-torch.set_default_dtype(torch.float64)
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 MIB = 2.0 ** 20
 
@@ -137,8 +136,8 @@ def test_network_gradient_matches_torch_autograd(oracle_lib, arch, C, H, W, clas
     x, y = wl.batch(b, C, H, W, classes, seed=5)
     loss, g = oracle.learner_grad(m, w0, x, y)
 
-    wt = torch.tensor(w0.astype(np.float64), requires_grad=True)
-    logits = TORCH_NETS[arch](Cursor(wt, layout), torch.tensor(x.astype(np.float64)))
+    wt = torch.tensor(w0.astype(np.float64), dtype=torch.float64, requires_grad=True)
+    logits = TORCH_NETS[arch](Cursor(wt, layout), torch.tensor(x.astype(np.float64), dtype=torch.float64))
     lt = F.cross_entropy(logits, torch.tensor(y, dtype=torch.long))
     lt.backward()
     assert abs(loss - lt.item()) < 1e-10 * max(1.0, abs(loss))
