@@ -187,9 +187,11 @@ class SMA:
         return lib().cbref_sma_apply(self._c, _ptr(g))
 
     def set_state(self, W, Z, Zp, Wprev=None):
+        # every converted array is held in a local until the call returns
         W = _f64(W).reshape(self.k, self.P)
         Wp = None if Wprev is None else _f64(Wprev).reshape(self.k, self.P)
-        lib().cbref_set_state(self._c, _ptr(W), _ptr(Wp), _ptr(_f64(Z)), _ptr(_f64(Zp)))
+        Z, Zp = _f64(Z), _f64(Zp)
+        lib().cbref_set_state(self._c, _ptr(W), _ptr(Wp), _ptr(Z), _ptr(Zp))
 
     def central(self):
         o = np.empty(self.P)
@@ -244,7 +246,8 @@ def batchnorm(x, gamma, beta, dy=None):
     dg = np.empty(C) if dy is not None else None
     dbt = np.empty(C) if dy is not None else None
     dyc = None if dy is None else _f64(dy)
-    lib().cbref_batchnorm(_ptr(x), N, C, HW, _ptr(_f64(gamma)), _ptr(_f64(beta)), _ptr(y),
+    gamma, beta = _f64(gamma), _f64(beta)
+    lib().cbref_batchnorm(_ptr(x), N, C, HW, _ptr(gamma), _ptr(beta), _ptr(y),
                           _ptr(dyc), _ptr(dx), _ptr(dg), _ptr(dbt))
     return y, dx, dg, dbt
 

@@ -238,9 +238,16 @@ def test_resnet32_k4_b32_full_size_learners():
 
 
 def test_resnet50_small_images():
-    p = Pair("resnet50", 3, 32, 32, 20, k=2, b=4, seed=2)
+    """Every ResNet-50 path (projection shortcuts, 7x7/2 stem, 3x3/2 max
+    pool, bottlenecks) on 64x64 images, 2 per learner.  Smaller inputs leave
+    batch norm over 4 values at the last stage, where fp32 inputs lose
+    their precision (the oracle's conditioning factor is 60 at 32x32 and 7
+    here).  No seed of this size makes every ReLU decision unambiguous
+    (best margin 1.5e-6 over 52 seeds), so the gradients take the
+    ambiguity bound; loss and state are strict."""
+    p = Pair("resnet50", 3, 64, 64, 20, k=2, b=2, seed=26)
     p.step(0)
-    p.check_grads()
+    p.check_grads(require_margin=False)
     p.sync()
     p.check_state()
 
@@ -276,8 +283,13 @@ def test_error_paths():
     ctx.cb_step(_dev(x), _dev(y))
     loss = ctx.cb_get_loss()
     assert np.isfinite(loss[0]) and np.isnan(loss[1])
-    # an infinite gradient makes z non-finite: reported by check_finite
+    # An infinite gradient sends the replicas to -inf at once, but z only
+    # at the next sync (corrections come from the replicas before their
+    # update); check_finite reports it then.
     g = torch.full((2, P), float("inf"), dtype=torch.float32, device="cuda")
+    ctx.cb_sma_apply(g)
+    assert np.isfinite(ctx.cb_get_central()).all()
+    assert not np.isfinite(ctx.cb_get_replica(0)).all()
     with pytest.raises(cb.CBError) as e:
-        ctx.cb_sma_apply(g)
+        ctx.cb_sma_apply(torch.zeros((2, P), dtype=torch.float32, device="cuda"))
     assert e.value.code == cb.CB_ENONFINITE
