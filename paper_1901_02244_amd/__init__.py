@@ -174,9 +174,10 @@ class Context:
         return rc
 
     def close(self):
-        if getattr(self, "_c", None):
-            lib().cb_destroy(self._c)
-            self._c = None
+        # at interpreter exit the module globals may already be gone
+        if getattr(self, "_c", None) and _lib is not None:
+            _lib.cb_destroy(self._c)
+        self._c = None
 
     __del__ = close
 

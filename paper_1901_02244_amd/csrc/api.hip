@@ -40,12 +40,14 @@ struct Op {
   bool bias = false, relu = false, need_dx = true;
   int64_t w_off = -1, b_off = -1;   // parameter offsets (elements)
   int splits = 1, chunk = 0;
+  bool emit_stats = false;          // epilogue writes BN partial sums
   // batch norm
   int C = 0;
   int64_t g_off = -1;
   int res = -1, res_mode = RES_NONE, res_st = 1;
   int64_t mean = -1, istd = -1, dres = -1;
   int chunks = 1;
+  int parts = 0;                    // > 0: statistics come from the producing conv
   // pooling
   int K = 0;
   int64_t arg = -1;
@@ -337,6 +339,16 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p) {
     x.act = take(bytes);
     x.grad = take(bytes);
   }
+  // a batch norm right after the conv that produces its input takes its
+  // statistics from that conv's epilogue
+  for (size_t i = 1; i < p.ops.size(); ++i) {
+    Op& o = p.ops[i];
+    Op& prev = p.ops[i - 1];
+    if (o.kind == OP_BN && prev.kind == OP_CONV && prev.out == o.in) {
+      prev.emit_stats = true;
+      o.parts = conv_fwd_tiles_m(geom(p, prev));
+    }
+  }
   int64_t bnpart = 0, split = 0;
   for (size_t i = 0; i < p.ops.size(); ++i) {
     Op& o = p.ops[i];
@@ -350,7 +362,7 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p) {
       o.mean = take((int64_t)k * o.C * 4);
       o.istd = take((int64_t)k * o.C * 4);
       o.chunks = bn_chunks(b, o.H * o.W, o.C, k);
-      bnpart = std::max<int64_t>(bnpart, (int64_t)k * o.C * o.chunks * 2 * 8);
+      bnpart = std::max<int64_t>(bnpart, (int64_t)k * o.C * std::max(o.chunks, o.parts) * 2 * 8);
       if (o.res >= 0) {
         const Tensor& r = p.t[o.res];
         if (r.consumers == 1) o.dres = r.grad;
@@ -488,6 +500,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         a.pstride = p.Pp;
         a.y = act(o.out);
         a.relu = o.relu;
+        a.stats = o.emit_stats ? c->at<double>(p.off_bnpart) : nullptr;
         const double flops = 2.0 * N * o.Ho * o.Wo * o.Co * o.Ci * o.R * o.R;
         const double bytes = 4.0 * ((double)N * o.Ci * o.H * o.W + (double)k * o.Co * o.Ci * o.R * o.R +
                                     (double)N * o.Co * o.Ho * o.Wo);
@@ -508,6 +521,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         a.istd = c->at<float>(o.istd);
         a.part = c->at<double>(p.off_bnpart);
         a.chunks = o.chunks;
+        a.parts = o.parts > 0 ? o.parts : o.chunks;
         a.relu = o.relu;
         a.res = o.res >= 0 ? act(o.res) : nullptr;
         a.res_mode = o.res >= 0 ? o.res_mode : RES_NONE;
@@ -518,7 +532,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         const double n = (double)N * o.C * o.H * o.W;
         const double res = a.res_mode == RES_SAME ? n
                            : a.res_mode == RES_SUBSAMPLE ? (double)N * a.res_C * o.H * o.W : 0.0;
-        CB_LAUNCH(c, "bn_stats_k", 0.0, 4.0 * n, bn_fwd_stats(a, s));
+        if (o.parts == 0) CB_LAUNCH(c, "bn_stats_k", 0.0, 4.0 * n, bn_fwd_stats(a, s));
         CB_LAUNCH(c, "bn_apply_k", 0.0, 4.0 * (2.0 * n + res), bn_fwd_apply(a, s));
         break;
       }

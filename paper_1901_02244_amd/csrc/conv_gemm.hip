@@ -11,15 +11,15 @@
 // replicas: one launch covers all learners and fills the CUs even when each
 // learner's batch is small (Sec. 3.1: learners train independently).
 //
-// Tiling: 256 threads (4 wave64s), LDS stages of BK = 16 contraction steps
+// Tiling: 256 threads (4 wave64s), LDS stages of BK contraction steps
 // stored with k contiguous, so each 16x16x4 MFMA operand group is one
-// ds_read_b128; the contraction index seen by lane l at sub-step kk is
-// 4*(l/16) + kk for both operands.  Global loads for the next stage are in
-// flight while the current stage is multiplied (two LDS buffers, one barrier
-// per stage).  The filter size R is a template parameter, so splitting a
-// contraction index into (channel, r, s) is multiply-shift arithmetic; in the
-// A-operand loaders that index is wave-uniform and the split runs on the
-// scalar unit.
+// ds_read_b128; within a group of 16 steps the contraction index seen by
+// lane l at sub-step kk is 4*(l/16) + kk for both operands.  Global loads
+// for the next stage are in flight while the current stage is multiplied
+// (two LDS buffers, one barrier per stage).  The filter size R is a template
+// parameter, so splitting a contraction index into (channel, r, s) is
+// multiply-shift arithmetic; in the A-operand loaders that index is
+// wave-uniform and the split runs on the scalar unit.
 #include "kernels.hpp"
 
 #include <algorithm>
@@ -29,42 +29,50 @@ namespace cbk {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
-constexpr int BK = 16;        // contraction steps per LDS stage
-constexpr int LDK = BK + 4;   // LDS row stride in floats (16-byte aligned rows)
 constexpr int OUT_OF_RANGE = -(1 << 29);
 
 __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// One LDS stage: As[rows][LDK], Bs[cols][LDK], both k-contiguous.
-template <int TM, int TN>
+// One LDS stage: As[rows][BK+4], Bs[cols][BK+4], both k-contiguous.
+template <int TM, int TN, int BK>
 __device__ __forceinline__ void mma_stage(const float* As, const float* Bs, int wm0, int wn0,
                                           int lane, v4f (&acc)[TM][TN]) {
+  constexpr int LDK = BK + 4;
   const int r = lane & 15, q = (lane >> 4) * 4;
-  v4f av[TM], bv[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) av[i] = *reinterpret_cast<const v4f*>(As + (wm0 + i * 16 + r) * LDK + q);
+  for (int g = 0; g < BK; g += 16) {
+    v4f av[TM], bv[TN];
 #pragma unroll
-  for (int i = 0; i < TN; ++i) bv[i] = *reinterpret_cast<const v4f*>(Bs + (wn0 + i * 16 + r) * LDK + q);
+    for (int i = 0; i < TM; ++i)
+      av[i] = *reinterpret_cast<const v4f*>(As + (wm0 + i * 16 + r) * LDK + g + q);
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk)
+    for (int i = 0; i < TN; ++i)
+      bv[i] = *reinterpret_cast<const v4f*>(Bs + (wn0 + i * 16 + r) * LDK + g + q);
 #pragma unroll
-    for (int a = 0; a < TM; ++a)
+    for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-      for (int b = 0; b < TN; ++b) acc[a][b] = mfma4(av[a][kk], bv[b][kk], acc[a][b]);
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) acc[a][b] = mfma4(av[a][kk], bv[b][kk], acc[a][b]);
+  }
 }
 
 __device__ __forceinline__ float relu0(float v) { return v > 0.f ? v : 0.f; }
 
+__device__ __forceinline__ double shfl_xor_d(double v, int o) { return __shfl_xor(v, o, 64); }
+
 // ---------------------------------------------------------------- forward
-template <int BM, int BN, int WM, int WN, int R>
+template <int BM, int BN, int WM, int WN, int R, int BK>
 __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   constexpr int RS = R * R;
+  constexpr int LDK = BK + 4;
   constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
   constexpr int TPR = 256 / BM;   // threads sharing one output row
   constexpr int KPT = BK / TPR;   // contraction steps each of them loads
-  constexpr int BQ = BN * (BK / 4);
+  constexpr int QPR = BK / 4;     // float4 groups per B row
+  constexpr int BQ = BN * QPR;
   constexpr int BPT = (BQ + 255) / 256;
   __shared__ __attribute__((aligned(16))) float As[2][BM * LDK];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDK];
@@ -109,7 +117,7 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   auto loadB = [&](int k0) {
 #pragma unroll
     for (int u = 0; u < BPT; ++u) {
-      const int idx = tid + u * 256, n = n0 + (idx >> 2), kq = k0 + 4 * (idx & 3);
+      const int idx = tid + u * 256, n = n0 + idx / QPR, kq = k0 + 4 * (idx % QPR);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         rb[u][i] = (idx < BQ && n < N && kq + i < K) ? Wt[(int64_t)n * K + kq + i] : 0.f;
@@ -124,7 +132,7 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
     for (int u = 0; u < BPT; ++u) {
       const int idx = tid + u * 256;
       if (idx < BQ)
-        *reinterpret_cast<v4f*>(&Bs[buf][(idx >> 2) * LDK + 4 * (idx & 3)]) =
+        *reinterpret_cast<v4f*>(&Bs[buf][(idx / QPR) * LDK + 4 * (idx % QPR)]) =
             v4f{rb[u][0], rb[u][1], rb[u][2], rb[u][3]};
     }
   };
@@ -134,7 +142,7 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   for (int x = 0; x < TM; ++x)
 #pragma unroll
     for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
-  const int wm0 = (wave % WM) * TM * 16, wn0 = (wave / WM) * TN * 16;
+  const int wm = wave % WM, wm0 = wm * TM * 16, wn0 = (wave / WM) * TN * 16;
   const int T = (K + BK - 1) / BK;
   loadA(0);
   loadB(0);
@@ -146,13 +154,16 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
       loadA((t + 1) * BK);
       loadB((t + 1) * BK);
     }
-    mma_stage<TM, TN>(As[cur], Bs[cur], wm0, wn0, lane, acc);
+    mma_stage<TM, TN, BK>(As[cur], Bs[cur], wm0, wn0, lane, acc);
     if (t + 1 < T) store(cur ^ 1);
     __syncthreads();
   }
 
   const float* bias = a.bias ? a.bias + (int64_t)j * a.pstride : nullptr;
   float* Y = a.y + (int64_t)j * g.b * N * HoWo;
+  double s1[TN], s2[TN];  // per-column sums of the stored outputs (BN statistics)
+#pragma unroll
+  for (int y = 0; y < TN; ++y) s1[y] = s2[y] = 0.0;
 #pragma unroll
   for (int x = 0; x < TM; ++x)
 #pragma unroll
@@ -168,6 +179,8 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
           float v = acc[x][y][i] + bv;
           if (a.relu) v = relu0(v);
           Y[((int64_t)img * N + n) * HoWo + p] = v;
+          s1[y] += (double)v;
+          s2[y] += (double)v * v;
         }
         if (++p == HoWo) {
           p = 0;
@@ -175,16 +188,48 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
         }
       }
     }
+  if (!a.stats) return;
+  // Per-channel partial sums of this tile for the batch norm that follows:
+  // lanes with the same column combine by an xor butterfly, then the WM
+  // waves of a column strip in wave order.  Written to
+  // stats[j][n][blockIdx.x][0..1].
+  __shared__ double red[WM][BN][2];
+#pragma unroll
+  for (int y = 0; y < TN; ++y) {
+    double u = s1[y], v = s2[y];
+    u += shfl_xor_d(u, 16);
+    v += shfl_xor_d(v, 16);
+    u += shfl_xor_d(u, 32);
+    v += shfl_xor_d(v, 32);
+    if (lane < 16) {
+      red[wm][wn0 + y * 16 + lane][0] = u;
+      red[wm][wn0 + y * 16 + lane][1] = v;
+    }
+  }
+  __syncthreads();
+  if (tid < BN && n0 + tid < N) {
+    double u = 0.0, v = 0.0;
+#pragma unroll
+    for (int w = 0; w < WM; ++w) {
+      u += red[w][tid][0];
+      v += red[w][tid][1];
+    }
+    double* o = a.stats + (((int64_t)j * N + n0 + tid) * gridDim.x + blockIdx.x) * 2;
+    o[0] = u;
+    o[1] = v;
+  }
 }
 
 // ------------------------------------------------------------ data grad
-template <int BM, int BN, int WM, int WN, int R, int ST>
+template <int BM, int BN, int WM, int WN, int R, int ST, int BK>
 __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   constexpr int RS = R * R;
+  constexpr int LDK = BK + 4;
   constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
   constexpr int TPR = 256 / BM;
   constexpr int KPT = BK / TPR;
-  constexpr int BQ = BN * (BK / 4);
+  constexpr int QPR = BK / 4;
+  constexpr int BQ = BN * QPR;
   constexpr int BPT = (BQ + 255) / 256;
   __shared__ __attribute__((aligned(16))) float As[2][BM * LDK];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDK];
@@ -236,7 +281,7 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   auto loadB = [&](int k0) {
 #pragma unroll
     for (int u = 0; u < BPT; ++u) {
-      const int idx = tid + u * 256, n = n0 + (idx >> 2), kq = k0 + 4 * (idx & 3);
+      const int idx = tid + u * 256, n = n0 + idx / QPR, kq = k0 + 4 * (idx % QPR);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float v = 0.f;
@@ -255,7 +300,7 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
     for (int u = 0; u < BPT; ++u) {
       const int idx = tid + u * 256;
       if (idx < BQ)
-        *reinterpret_cast<v4f*>(&Bs[buf][(idx >> 2) * LDK + 4 * (idx & 3)]) =
+        *reinterpret_cast<v4f*>(&Bs[buf][(idx / QPR) * LDK + 4 * (idx % QPR)]) =
             v4f{rb[u][0], rb[u][1], rb[u][2], rb[u][3]};
     }
   };
@@ -277,7 +322,7 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       loadA((t + 1) * BK);
       loadB((t + 1) * BK);
     }
-    mma_stage<TM, TN>(As[cur], Bs[cur], wm0, wn0, lane, acc);
+    mma_stage<TM, TN, BK>(As[cur], Bs[cur], wm0, wn0, lane, acc);
     if (t + 1 < T) store(cur ^ 1);
     __syncthreads();
   }
@@ -322,11 +367,16 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
 }
 
 // ---------------------------------------------------------- weight grad
-template <int BM, int BN, int WM, int WN, int R>
+// Stages of BK pixels; thread (pl, rg) loads pixel pl of the stage for the
+// dY rows rg, rg+RG, ... and the im2col rows (ci, r, s) rg, rg+RG, ...
+template <int BM, int BN, int WM, int WN, int R, int BK>
 __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
   constexpr int RS = R * R;
+  constexpr int LDK = BK + 4;
   constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
-  constexpr int RA = BM / 16, RB = BN / 16;  // rows each thread loads per stage
+  constexpr int RG = 256 / BK;            // row groups
+  constexpr int RA = BM / RG, RB = BN / RG;
+  static_assert(RA >= 1 && RB >= 1, "tile smaller than the row groups");
   __shared__ __attribute__((aligned(16))) float As[2][BM * LDK];
   __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDK];
 
@@ -340,7 +390,7 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
   const float* X = a.x + (int64_t)j * g.b * g.Ci * HW;
   const float* DY = a.dy + (int64_t)j * g.b * g.Co * HoWo;
 
-  const int pl = tid & 15, rg = tid >> 4;
+  const int pl = tid % BK, rg = tid / BK;
   // pixel this thread loads in the current stage, kept as (img, oh, ow)
   int pix = L0 + pl;
   int img = pix / HoWo, rem = pix - img * HoWo, oh = rem / g.Wo, ow = rem - oh * g.Wo;
@@ -348,7 +398,7 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
   int tx[RB], tr[RB], ts[RB];
 #pragma unroll
   for (int i = 0; i < RB; ++i) {
-    const int kk = n0 + rg + 16 * i;
+    const int kk = n0 + rg + RG * i;
     const int ci = kk / RS, rs = kk - ci * RS, r = rs / R, s = rs - r * R;
     tx[i] = ci * HW + r * g.W + s;
     tr[i] = kk < No ? r : OUT_OF_RANGE;
@@ -363,7 +413,7 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
     const int xb = img * g.Ci * HW + ih0 * g.W + iw0;
 #pragma unroll
     for (int i = 0; i < RA; ++i) {
-      const int co = m0 + rg + 16 * i;
+      const int co = m0 + rg + RG * i;
       ra[i] = (ok && co < Mo) ? DY[yb + co * HoWo] : 0.f;
     }
 #pragma unroll
@@ -387,9 +437,9 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
   };
   auto store = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < RA; ++i) As[buf][(rg + 16 * i) * LDK + pl] = ra[i];
+    for (int i = 0; i < RA; ++i) As[buf][(rg + RG * i) * LDK + pl] = ra[i];
 #pragma unroll
-    for (int i = 0; i < RB; ++i) Bs[buf][(rg + 16 * i) * LDK + pl] = rb[i];
+    for (int i = 0; i < RB; ++i) Bs[buf][(rg + RG * i) * LDK + pl] = rb[i];
   };
 
   v4f acc[TM][TN];
@@ -408,7 +458,7 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
       advance();
       load();
     }
-    mma_stage<TM, TN>(As[cur], Bs[cur], wm0, wn0, lane, acc);
+    mma_stage<TM, TN, BK>(As[cur], Bs[cur], wm0, wn0, lane, acc);
     if (t + 1 < T) store(cur ^ 1);
     __syncthreads();
   }
@@ -428,15 +478,24 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
     }
 }
 
+// dw[j][e] = sum over s of part[j][s][e], s in order.  A block covers 64
+// elements; its 4 waves take the splits in 4 contiguous runs, combined in
+// run order.
 __global__ __launch_bounds__(256) void reduce_splits_k(const float* part, int splits, int64_t n,
                                                        float* dw, int64_t pstride) {
-  const int j = blockIdx.y;
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= n) return;
-  const float* p = part + (int64_t)j * splits * n + e;
+  __shared__ float red[4][64];
+  const int j = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t e = (int64_t)blockIdx.x * 64 + lane;
+  const int per = (splits + 3) / 4, s0 = w * per, s1 = min(splits, s0 + per);
   float s = 0.f;
-  for (int i = 0; i < splits; ++i) s += p[(int64_t)i * n];
-  dw[(int64_t)j * pstride + e] = s;
+  if (e < n) {
+    const float* p = part + (int64_t)j * splits * n + e;
+    for (int i = s0; i < s1; ++i) s += p[(int64_t)i * n];
+  }
+  red[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && e < n)
+    dw[(int64_t)j * pstride + e] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -465,39 +524,48 @@ __global__ __launch_bounds__(256) void channel_sum_k(const float* dy, int b, int
 inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
 
 // Name of one kernel instantiation, as the profiler shows its template.
-template <int KIND, int BM, int BN, int WM, int WN, int R, int ST = 0>
+template <int KIND, int BM, int BN, int WM, int WN, int R, int ST, int BK>
 const char* tile_name() {
   static const char* base[3] = {"conv_fwd_k", "conv_bwd_data_k", "conv_bwd_weight_k"};
   static const std::string n = std::string(base[KIND]) + "<" + std::to_string(BM) + ", " +
                                std::to_string(BN) + ", " + std::to_string(WM) + ", " +
                                std::to_string(WN) + ", " + std::to_string(R) +
-                               (ST ? ", " + std::to_string(ST) : "") + ">";
+                               (ST ? ", " + std::to_string(ST) : "") + ", " +
+                               std::to_string(BK) + ">";
   return n.c_str();
 }
 
+// LDS stage depth: 32 contraction steps, except for 256-row tiles (16).
+template <int BM>
+constexpr int stage_k() { return BM >= 256 ? 16 : 32; }
+
 template <int BM, int BN, int WM, int WN, int R>
 hipError_t launch_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
+  constexpr int BK = stage_k<BM>();
   const int M = a.g.b * a.g.Ho * a.g.Wo;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Co, BN), a.g.k);
-  hipLaunchKernelGGL((conv_fwd_k<BM, BN, WM, WN, R>), grid, dim3(256), 0, s, a);
-  if (name) *name = tile_name<0, BM, BN, WM, WN, R>();
+  hipLaunchKernelGGL((conv_fwd_k<BM, BN, WM, WN, R, BK>), grid, dim3(256), 0, s, a);
+  if (name) *name = tile_name<0, BM, BN, WM, WN, R, 0, BK>();
   return hipGetLastError();
 }
 
 template <int BM, int BN, int WM, int WN, int R, int ST>
 hipError_t launch_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
+  constexpr int BK = stage_k<BM>();
   const int M = a.g.b * a.g.H * a.g.W;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Ci, BN), a.g.k);
-  hipLaunchKernelGGL((conv_bwd_data_k<BM, BN, WM, WN, R, ST>), grid, dim3(256), 0, s, a);
-  if (name) *name = tile_name<1, BM, BN, WM, WN, R, ST>();
+  hipLaunchKernelGGL((conv_bwd_data_k<BM, BN, WM, WN, R, ST, BK>), grid, dim3(256), 0, s, a);
+  if (name) *name = tile_name<1, BM, BN, WM, WN, R, ST, BK>();
   return hipGetLastError();
 }
+
+constexpr int WG_BK = 32;  // pixels per stage of the weight gradient
 
 template <int BM, int BN, int WM, int WN, int R>
 hipError_t launch_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char** name) {
   dim3 grid(cdiv(a.g.Co, BM), cdiv(a.g.Ci * R * R, BN), a.g.k * a.splits);
-  hipLaunchKernelGGL((conv_bwd_weight_k<BM, BN, WM, WN, R>), grid, dim3(256), 0, s, a);
-  if (name) *name = tile_name<2, BM, BN, WM, WN, R>();
+  hipLaunchKernelGGL((conv_bwd_weight_k<BM, BN, WM, WN, R, WG_BK>), grid, dim3(256), 0, s, a);
+  if (name) *name = tile_name<2, BM, BN, WM, WN, R, 0, WG_BK>();
   return hipGetLastError();
 }
 
@@ -515,6 +583,11 @@ int pick_tile(int64_t M, int N, int k) {
   if (N <= 16) return wgs(256, 16) >= MIN_WGS ? 0 : 1;
   if (N <= 32) return wgs(128, 32) >= MIN_WGS ? 2 : 3;
   return wgs(128, 64) >= MIN_WGS ? 4 : 5;
+}
+
+int tile_rows(int t) {
+  static const int rows[6] = {256, 64, 128, 64, 128, 64};
+  return rows[t];
 }
 
 template <int R>
@@ -552,13 +625,18 @@ hipError_t bwd_weight_r(const ConvBwdWeightArgs& a, hipStream_t s, const char** 
 
 }  // namespace
 
+int conv_fwd_tiles_m(const ConvGeom& g) {
+  const int64_t M = (int64_t)g.b * g.Ho * g.Wo;
+  return (int)cdiv(M, tile_rows(pick_tile(M, g.Co, g.k)));
+}
+
 int conv_bwd_weight_splits(const ConvGeom& g, int* chunk) {
   const int L = g.b * g.Ho * g.Wo;
   const int bm = bwd_weight_bm(g.Co);
   const int64_t tiles = (int64_t)cdiv(g.Co, bm) * cdiv(g.Ci * g.R * g.S, 64) * g.k;
-  int splits = (int)std::max<int64_t>(1, std::min<int64_t>(cdiv(L, 64), cdiv(1024, tiles)));
+  int splits = (int)std::max<int64_t>(1, std::min<int64_t>(cdiv(L, 2 * WG_BK), cdiv(1024, tiles)));
   int c = (int)cdiv(L, splits);
-  c = (c + BK - 1) / BK * BK;
+  c = (c + WG_BK - 1) / WG_BK * WG_BK;
   *chunk = c;
   return (int)cdiv(L, c);
 }
@@ -605,7 +683,7 @@ hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char
 
 hipError_t reduce_splits(const float* partial, int k, int splits, int64_t n, float* dw,
                          int64_t pstride, hipStream_t s) {
-  hipLaunchKernelGGL(reduce_splits_k, dim3(cdiv(n, 256), k), dim3(256), 0, s, partial, splits, n,
+  hipLaunchKernelGGL(reduce_splits_k, dim3(cdiv(n, 64), k), dim3(256), 0, s, partial, splits, n,
                      dw, pstride);
   return hipGetLastError();
 }

@@ -28,6 +28,10 @@ struct ConvFwdArgs {
   int64_t pstride;    // elements between replicas' parameters
   float* y;           // [k*b][Co][Ho][Wo]
   int relu;
+  // If not null: per-channel partial sums (sum, sum of squares) of the
+  // stored outputs of each M tile, [k][Co][tiles_m][2], for the batch norm
+  // that consumes y (tiles_m = conv_fwd_tiles_m).
+  double* stats;
 };
 
 // Residual added to a data gradient (the shortcut of a residual block):
@@ -62,6 +66,8 @@ struct ConvBwdWeightArgs {
 // Square filters R in {1, 3, 5, 7}, stride 1 or 2; the data gradient is
 // built for (R, stride) in {(1,1), (1,2), (3,1), (3,2), (5,1)}.
 bool conv_supported(int R, int S, int st, bool need_dx);
+// Number of M tiles of the forward GEMM (the partial-statistics count).
+int conv_fwd_tiles_m(const ConvGeom& g);
 // Split of the weight-gradient contraction; exposed so the host can size scratch.
 int conv_bwd_weight_splits(const ConvGeom& g, int* chunk);
 
@@ -89,8 +95,9 @@ struct BNArgs {
   int64_t pstride;
   float* mean;          // [k][C] saved for backward
   float* istd;          // [k][C]
-  double* part;         // scratch [k][C][chunks][2]
-  int chunks;
+  double* part;         // partial sums [k][C][parts][2]
+  int parts;            // partials per (replica, channel)
+  int chunks;           // blocks per (replica, channel) in the kernels' grids
   int relu;
   const float* res;     // residual input or nullptr
   int res_mode, res_C, res_st, res_H, res_W;
@@ -113,7 +120,8 @@ struct BNBwdArgs {
 };
 
 int bn_chunks(int b, int HW, int C, int k);
-// Forward: per-chunk fp64 sums, then normalise (+ residual, ReLU).
+// Forward: per-chunk fp64 sums (parts = chunks), then normalise (+ residual,
+// ReLU).  The sums can instead come from the producing conv's epilogue.
 hipError_t bn_fwd_stats(const BNArgs& a, hipStream_t s);
 hipError_t bn_fwd_apply(const BNArgs& a, hipStream_t s);
 // Backward: per-chunk fp64 sums of dy and dy*xhat, then dx (and dgamma/dbeta).

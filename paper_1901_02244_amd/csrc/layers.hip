@@ -85,16 +85,19 @@ __global__ __launch_bounds__(256) void bn_stats_k(BNArgs a) {
 }
 
 __global__ __launch_bounds__(256) void bn_apply_k(BNArgs a) {
+  __shared__ double red[8];
   const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
   const int HW = a.H * a.W, n = a.b * HW;
   const int per = (n + a.chunks - 1) / a.chunks;
   const int e0 = chunk * per, e1 = min(n, e0 + per);
-  const double* p = a.part + ((int64_t)j * a.C + c) * a.chunks * 2;
+  // the partial sums of this (replica, channel), combined in a fixed order
+  const double* p = a.part + ((int64_t)j * a.C + c) * a.parts * 2;
   double s = 0.0, ss = 0.0;
-  for (int i = 0; i < a.chunks; ++i) {
+  for (int i = threadIdx.x; i < a.parts; i += 256) {
     s += p[2 * i];
     ss += p[2 * i + 1];
   }
+  block_sum2(s, ss, red);
   const double mean = s / n;
   const double var = fmax(ss / n - mean * mean, 0.0);
   const float mf = (float)mean, isf = (float)(1.0 / sqrt(var + BN_EPS));

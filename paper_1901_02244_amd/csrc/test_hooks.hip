@@ -65,6 +65,7 @@ int cb_test_conv(int k, int b, int Ci, int H, int W, int Co, int R, int stride, 
   f.pstride = pstride;
   f.y = y;
   f.relu = relu;
+  f.stats = nullptr;
   int rc = rc_of(conv_fwd(f, s));
   if (rc || !dy) return rc;
   if (!grads) return CB_EINVAL;
@@ -120,6 +121,7 @@ int cb_test_bn_fwd(int k, int b, int C, int H, int W, int relu, const float* x,
   a.istd = istd;
   a.part = static_cast<double*>(scratch);
   a.chunks = bn_chunks(b, H * W, C, k);
+  a.parts = a.chunks;
   a.relu = relu;
   a.res = nullptr;
   a.res_mode = RES_NONE;

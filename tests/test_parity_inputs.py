@@ -27,17 +27,6 @@ def test_strict_inputs_have_unambiguous_decisions(oracle_lib, arch, shape, class
         assert margin >= MARGIN, (arch, j, margin)
 
 
-def test_resnet50_parity_input_is_well_conditioned(oracle_lib):
-    """The ResNet-50 end-to-end case (64x64 images, 2 per learner, seed 26)
-    keeps every batch norm's conditioning factor below 10."""
-    m = oracle.model("resnet50", 3, 64, 64, 20)
-    w0 = wl.init_w0(oracle.tensors(m), 26)
-    x, y = wl.batch(4, 3, 64, 64, 20, 26, 0)
-    for j in range(2):
-        _, cond = oracle.learner_margin(m, w0, x[2 * j:2 * j + 2], y[2 * j:2 * j + 2], with_bn=True)
-        assert cond < 10.0, (j, cond)
-
-
 def test_margin_detects_a_decision_at_zero(oracle_lib):
     """A ReLU input that is exactly zero (a blank patch under a zero bias)
     gives margin 0; the same image without the patch does not."""
