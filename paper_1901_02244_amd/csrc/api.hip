@@ -41,6 +41,7 @@ struct Op {
   int64_t w_off = -1, b_off = -1;   // parameter offsets (elements)
   int splits = 1, chunk = 0;
   bool emit_stats = false;          // epilogue writes BN partial sums
+  int bnb = -1;                     // data-gradient epilogue feeds this BN's backward sums
   // batch norm
   int C = 0;
   int64_t g_off = -1;
@@ -48,6 +49,7 @@ struct Op {
   int64_t mean = -1, istd = -1, dres = -1;
   int chunks = 1;
   int parts = 0;                    // > 0: statistics come from the producing conv
+  int bwd_parts = 0;                // > 0: backward sums come from the next conv's dx
   // pooling
   int K = 0;
   int64_t arg = -1;
@@ -349,6 +351,29 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p) {
       o.parts = conv_fwd_tiles_m(geom(p, prev));
     }
   }
+  // a batch norm whose output gradient is written last by the data
+  // gradient of the very next conv takes its backward sums from that
+  // conv's epilogue (nothing else touches the partial-sum scratch between
+  // the two)
+  {
+    std::vector<int> writer(p.t.size(), -1);
+    for (int i = (int)p.ops.size() - 1; i >= 0; --i) {
+      const Op& o = p.ops[i];
+      if ((o.kind == OP_CONV && o.need_dx) || o.kind == OP_GAP || o.kind == OP_MAXPOOL ||
+          o.kind == OP_BN)
+        writer[o.in] = i;
+      if (o.kind == OP_BN && o.res >= 0 && p.t[o.res].consumers == 1) writer[o.res] = i;
+    }
+    for (size_t i = 0; i + 1 < p.ops.size(); ++i) {
+      Op& o = p.ops[i];
+      Op& w = p.ops[i + 1];
+      if (o.kind == OP_BN && writer[o.out] == (int)i + 1 && w.kind == OP_CONV && w.need_dx &&
+          w.in == o.out && !w.dx_mask) {
+        w.bnb = (int)i;
+        o.bwd_parts = conv_bwd_data_tiles_m(geom(p, w));
+      }
+    }
+  }
   int64_t bnpart = 0, split = 0;
   for (size_t i = 0; i < p.ops.size(); ++i) {
     Op& o = p.ops[i];
@@ -362,7 +387,8 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p) {
       o.mean = take((int64_t)k * o.C * 4);
       o.istd = take((int64_t)k * o.C * 4);
       o.chunks = bn_chunks(b, o.H * o.W, o.C, k);
-      bnpart = std::max<int64_t>(bnpart, (int64_t)k * o.C * std::max(o.chunks, o.parts) * 2 * 8);
+      bnpart = std::max<int64_t>(
+          bnpart, (int64_t)k * o.C * std::max(std::max(o.chunks, o.parts), o.bwd_parts) * 2 * 8);
       if (o.res >= 0) {
         const Tensor& r = p.t[o.res];
         if (r.consumers == 1) o.dres = r.grad;
@@ -583,9 +609,11 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         a.istd = c->at<float>(o.istd);
         a.part = c->at<double>(p.off_bnpart);
         a.chunks = o.chunks;
+        a.parts = o.bwd_parts > 0 ? o.bwd_parts : o.chunks;
         const double n = (double)N * o.C * o.H * o.W;
         const double mask = o.relu ? 1.0 : 0.0, dres = o.res >= 0 ? 1.0 : 0.0;
-        CB_LAUNCH(c, "bn_bwd_stats_k", 0.0, 4.0 * n * (2.0 + mask), bn_bwd_stats(a, s));
+        if (o.bwd_parts == 0)
+          CB_LAUNCH(c, "bn_bwd_stats_k", 0.0, 4.0 * n * (2.0 + mask), bn_bwd_stats(a, s));
         CB_LAUNCH(c, "bn_bwd_apply_k", 0.0, 4.0 * n * (3.0 + mask + dres), bn_bwd_apply(a, s));
         break;
       }
@@ -629,6 +657,16 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
           d.add_mode = o.add_mode;
           d.add_C = o.add_C;
           d.add_st = o.add_st;
+          d.bn_part = nullptr;
+          d.bn_x = d.bn_y = d.bn_mean = d.bn_istd = nullptr;
+          if (o.bnb >= 0) {
+            const Op& bn = p.ops[o.bnb];
+            d.bn_part = c->at<double>(p.off_bnpart);
+            d.bn_x = act(bn.in);
+            d.bn_y = bn.relu ? act(bn.out) : nullptr;
+            d.bn_mean = c->at<float>(bn.mean);
+            d.bn_istd = c->at<float>(bn.istd);
+          }
           ProfScope ps(c);
           const char* nm = "conv_bwd_data_k";
           CB_HIP(c, conv_bwd_data(d, s, &nm));

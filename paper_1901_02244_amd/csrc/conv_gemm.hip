@@ -334,6 +334,12 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   if (ADD)
     ADD += (a.add_mode == ADD_SAME) ? (int64_t)j * g.b * N * HW
                                     : (int64_t)j * g.b * a.add_C * Hs * Ws;
+  const bool bn = a.bn_part != nullptr;
+  const float* BX = bn ? a.bn_x + (int64_t)j * g.b * N * HW : nullptr;
+  const float* BY = (bn && a.bn_y) ? a.bn_y + (int64_t)j * g.b * N * HW : nullptr;
+  double s1[TN], s2[TN];
+#pragma unroll
+  for (int y = 0; y < TN; ++y) s1[y] = s2[y] = 0.0;
 #pragma unroll
   for (int x = 0; x < TM; ++x)
 #pragma unroll
@@ -342,6 +348,11 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       const int mb = m0 + wm0 + x * 16 + (lane >> 4) * 4;
       if (n >= N || mb >= M) continue;
       int img = mb / HW, p = mb - img * HW;
+      float bm = 0.f, bi = 0.f;
+      if (bn) {
+        bm = a.bn_mean[j * N + n];
+        bi = a.bn_istd[j * N + n];
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         if (mb + i < M) {
@@ -357,6 +368,12 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
           }
           if (MSK && !(MSK[idx] > 0.f)) v = 0.f;
           DX[idx] = v;
+          if (bn) {
+            const float d = (BY && !(BY[idx] > 0.f)) ? 0.f : v;
+            const float xh = (BX[idx] - bm) * bi;
+            s1[y] += (double)d;
+            s2[y] += (double)d * xh;
+          }
         }
         if (++p == HW) {
           p = 0;
@@ -364,6 +381,35 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
         }
       }
     }
+  if (!bn) return;
+  // per-channel partial sums of this tile, combined in a fixed order (lanes
+  // of a column by xor butterfly, then the WM waves of a column strip)
+  __shared__ double red[WM][BN][2];
+  const int wm = wave % WM;
+#pragma unroll
+  for (int y = 0; y < TN; ++y) {
+    double u = s1[y], w = s2[y];
+    u += shfl_xor_d(u, 16);
+    w += shfl_xor_d(w, 16);
+    u += shfl_xor_d(u, 32);
+    w += shfl_xor_d(w, 32);
+    if (lane < 16) {
+      red[wm][wn0 + y * 16 + lane][0] = u;
+      red[wm][wn0 + y * 16 + lane][1] = w;
+    }
+  }
+  __syncthreads();
+  if (tid < BN && n0 + tid < N) {
+    double u = 0.0, w = 0.0;
+#pragma unroll
+    for (int q = 0; q < WM; ++q) {
+      u += red[q][tid][0];
+      w += red[q][tid][1];
+    }
+    double* o = a.bn_part + (((int64_t)j * N + n0 + tid) * gridDim.x + blockIdx.x) * 2;
+    o[0] = u;
+    o[1] = w;
+  }
 }
 
 // ---------------------------------------------------------- weight grad
@@ -628,6 +674,11 @@ hipError_t bwd_weight_r(const ConvBwdWeightArgs& a, hipStream_t s, const char** 
 int conv_fwd_tiles_m(const ConvGeom& g) {
   const int64_t M = (int64_t)g.b * g.Ho * g.Wo;
   return (int)cdiv(M, tile_rows(pick_tile(M, g.Co, g.k)));
+}
+
+int conv_bwd_data_tiles_m(const ConvGeom& g) {
+  const int64_t M = (int64_t)g.b * g.H * g.W;
+  return (int)cdiv(M, tile_rows(pick_tile(M, g.Ci, g.k)));
 }
 
 int conv_bwd_weight_splits(const ConvGeom& g, int* chunk) {

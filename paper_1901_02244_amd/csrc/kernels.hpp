@@ -51,6 +51,15 @@ struct ConvBwdDataArgs {
   const float* mask;  // zero dx where mask <= 0 (a fused ReLU upstream), or nullptr
   const float* add;   // residual gradient, or nullptr
   int add_mode, add_C, add_st;
+  // If bn_part is not null, dx is the output gradient of a batch norm; the
+  // epilogue also writes that norm's backward partial sums per M tile:
+  // with d = dx masked where bn_y <= 0 (bn_y may be null) and
+  // xh = (bn_x - mean) * istd: sum d and sum d*xh, [k][Ci][tiles_m][2].
+  double* bn_part;
+  const float* bn_x;
+  const float* bn_y;
+  const float* bn_mean;
+  const float* bn_istd;
 };
 
 struct ConvBwdWeightArgs {
@@ -66,8 +75,10 @@ struct ConvBwdWeightArgs {
 // Square filters R in {1, 3, 5, 7}, stride 1 or 2; the data gradient is
 // built for (R, stride) in {(1,1), (1,2), (3,1), (3,2), (5,1)}.
 bool conv_supported(int R, int S, int st, bool need_dx);
-// Number of M tiles of the forward GEMM (the partial-statistics count).
+// Number of M tiles of the forward / data-gradient GEMMs (the counts of the
+// batch-norm partial sums their epilogues write).
 int conv_fwd_tiles_m(const ConvGeom& g);
+int conv_bwd_data_tiles_m(const ConvGeom& g);
 // Split of the weight-gradient contraction; exposed so the host can size scratch.
 int conv_bwd_weight_splits(const ConvGeom& g, int* chunk);
 
@@ -115,7 +126,8 @@ struct BNBwdArgs {
   int64_t pstride;
   const float* mean;
   const float* istd;
-  double* part;
+  double* part;         // partial sums [k][C][parts][2]
+  int parts;
   int chunks;
 };
 
@@ -124,7 +136,9 @@ int bn_chunks(int b, int HW, int C, int k);
 // ReLU).  The sums can instead come from the producing conv's epilogue.
 hipError_t bn_fwd_stats(const BNArgs& a, hipStream_t s);
 hipError_t bn_fwd_apply(const BNArgs& a, hipStream_t s);
-// Backward: per-chunk fp64 sums of dy and dy*xhat, then dx (and dgamma/dbeta).
+// Backward: per-chunk fp64 sums of dy and dy*xhat (parts = chunks), then dx
+// and dgamma/dbeta.  The sums can instead come from the epilogue of the
+// data-gradient GEMM that wrote dy.
 hipError_t bn_bwd_stats(const BNBwdArgs& a, hipStream_t s);
 hipError_t bn_bwd_apply(const BNBwdArgs& a, hipStream_t s);
 

@@ -156,16 +156,18 @@ __global__ __launch_bounds__(256) void bn_bwd_stats_k(BNBwdArgs a) {
 }
 
 __global__ __launch_bounds__(256) void bn_bwd_apply_k(BNBwdArgs a) {
+  __shared__ double red[8];
   const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
   const int HW = a.H * a.W, n = a.b * HW;
   const int per = (n + a.chunks - 1) / a.chunks;
   const int e0 = chunk * per, e1 = min(n, e0 + per);
-  const double* p = a.part + ((int64_t)j * a.C + c) * a.chunks * 2;
+  const double* p = a.part + ((int64_t)j * a.C + c) * a.parts * 2;
   double s = 0.0, sx = 0.0;
-  for (int i = 0; i < a.chunks; ++i) {
+  for (int i = threadIdx.x; i < a.parts; i += 256) {
     s += p[2 * i];
     sx += p[2 * i + 1];
   }
+  block_sum2(s, sx, red);
   const float mf = a.mean[j * a.C + c], isf = a.istd[j * a.C + c];
   const float ga = a.gamma[(int64_t)j * a.pstride + c];
   if (chunk == 0 && threadIdx.x == 0) {

@@ -97,6 +97,8 @@ int cb_test_conv(int k, int b, int Ci, int H, int W, int Co, int R, int stride, 
   d.add_mode = ADD_NONE;
   d.add_C = 0;
   d.add_st = 1;
+  d.bn_part = nullptr;
+  d.bn_x = d.bn_y = d.bn_mean = d.bn_istd = nullptr;
   return rc_of(conv_bwd_data(d, s));
 }
 
@@ -154,6 +156,7 @@ int cb_test_bn_bwd(int k, int b, int C, int H, int W, const float* x, const floa
   a.istd = istd;
   a.part = static_cast<double*>(scratch);
   a.chunks = bn_chunks(b, H * W, C, k);
+  a.parts = a.chunks;
   int rc = rc_of(bn_bwd_stats(a, s));
   if (rc) return rc;
   return rc_of(bn_bwd_apply(a, s));
