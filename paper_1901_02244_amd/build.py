@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcrossbow_sma.so")
-SOURCES = ["api.hip", "conv_gemm.hip", "layers.hip", "sma.hip", "test_hooks.hip"]
+SOURCES = ["api.hip", "conv_gemm.hip", "conv_direct.hip", "layers.hip", "sma.hip", "test_hooks.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -672,11 +672,13 @@ hipError_t bwd_weight_r(const ConvBwdWeightArgs& a, hipStream_t s, const char** 
 }  // namespace
 
 int conv_fwd_tiles_m(const ConvGeom& g) {
+  if (conv_direct_fwd_ok(g)) return conv_direct_fwd_tiles(g);
   const int64_t M = (int64_t)g.b * g.Ho * g.Wo;
   return (int)cdiv(M, tile_rows(pick_tile(M, g.Co, g.k)));
 }
 
 int conv_bwd_data_tiles_m(const ConvGeom& g) {
+  if (conv_direct_bwd_data_ok(g)) return conv_direct_bwd_data_tiles(g);
   const int64_t M = (int64_t)g.b * g.H * g.W;
   return (int)cdiv(M, tile_rows(pick_tile(M, g.Ci, g.k)));
 }
@@ -701,6 +703,7 @@ bool conv_supported(int R, int S, int st, bool need_dx) {
 }
 
 hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
+  if (conv_direct_fwd_ok(a.g)) return conv_direct_fwd(a, s, name);
   switch (a.g.R) {
     case 1: return fwd_r<1>(a, s, name);
     case 3: return fwd_r<3>(a, s, name);
@@ -711,6 +714,7 @@ hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
 }
 
 hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
+  if (conv_direct_bwd_data_ok(a.g)) return conv_direct_bwd_data(a, s, name);
   const int key = a.g.R * 10 + a.g.st;
   switch (key) {
     case 11: return bwd_data_r<1, 1>(a, s, name);

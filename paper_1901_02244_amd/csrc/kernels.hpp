@@ -88,6 +88,18 @@ hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name = nul
 hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name = nullptr);
 hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s,
                            const char** name = nullptr);
+// 3x3 stride-1 pad-1 convolutions on 8/16/32-wide square images with
+// channel counts that are multiples of 16 run on a direct kernel (input
+// tile staged once in LDS); conv_fwd / conv_bwd_data route there
+// themselves.  *_tiles give its number of row tiles per replica (the count
+// of batch-norm partial sums its epilogue writes).
+bool conv_direct_fwd_ok(const ConvGeom& g);
+bool conv_direct_bwd_data_ok(const ConvGeom& g);
+int conv_direct_fwd_tiles(const ConvGeom& g);
+int conv_direct_bwd_data_tiles(const ConvGeom& g);
+hipError_t conv_direct_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name = nullptr);
+hipError_t conv_direct_bwd_data(const ConvBwdDataArgs& a, hipStream_t s,
+                                const char** name = nullptr);
 // dw[j][e] = sum over splits of partial[j][s][e], s in order.
 hipError_t reduce_splits(const float* partial, int k, int splits, int64_t n, float* dw,
                          int64_t pstride, hipStream_t s);

@@ -52,6 +52,15 @@ CONV = [
     ("r50.s4.b", 2, 32, 512, 7, 512, 3, 1, 1, 0, 0, 1),
     ("r50.s4.a2", 2, 32, 2048, 7, 512, 1, 1, 0, 0, 0, 1),
     ("r50.fc", 2, 32, 2048, 1, 1000, 1, 1, 0, 0, 1, 1),
+    # 3x3 stride-1 layers of the direct kernel: every tile choice, bias and
+    # ReLU, channel counts that are not multiples of 32, k = 1 and k = 32
+    ("direct.w32.k1", 1, 16, 16, 32, 16, 3, 1, 1, 0, 0, 1),
+    ("direct.w32.bias", 2, 3, 16, 32, 16, 3, 1, 1, 1, 1, 1),
+    ("direct.w32.16to32", 2, 4, 16, 32, 32, 3, 1, 1, 1, 0, 1),
+    ("direct.w16.c48", 3, 2, 48, 16, 48, 3, 1, 1, 1, 1, 1),
+    ("direct.w16.k32", 32, 16, 32, 16, 32, 3, 1, 1, 0, 0, 1),
+    ("direct.w8.32to64", 1, 16, 32, 8, 64, 3, 1, 1, 0, 1, 1),
+    ("direct.w8.k32", 32, 16, 64, 8, 64, 3, 1, 1, 0, 0, 1),
     # ragged: partial tiles in every GEMM dimension
     ("ragged.3x3s2", 3, 5, 7, 13, 19, 3, 2, 1, 0, 0, 1),
     ("ragged.5x5", 2, 3, 5, 11, 37, 5, 1, 2, 1, 1, 1),
