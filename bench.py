@@ -86,16 +86,23 @@ def time_training(wk, steps, warmup, ring=8, prof_steps=0):
     loss = ctx.cb_get_loss()
     prof = None
     if prof_steps:
-        # per-kernel durations: every launch bracketed by events on the
-        # context's stream (a separate pass, so the timed loop is untouched)
+        # per-kernel durations: every launch carries start/stop events on its
+        # own dispatch (hipExtLaunchKernel), on the context's stream; the same
+        # loop as the timed one, run again with instrumentation on
         ctx.cb_profile_enable(True)
+        pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        pe0.record()
         for i in range(prof_steps):
             ctx.cb_step(xs[i % n], ys[i % n])
             ctx.cb_sync()
+        pe1.record()
+        torch.cuda.synchronize()
         prof = ctx.cb_profile()
         ctx.cb_profile_enable(False)
         prof = {k: (v[0] / prof_steps, v[1] / prof_steps, v[2] / prof_steps, v[3] / prof_steps)
                 for k, v in prof.items()}
+        log(f"[bench] {wk.name}: instrumented pass {pe0.elapsed_time(pe1) / prof_steps:.3f} ms/step "
+            f"(kernel sum {sum(v[1] for v in prof.values()):.3f} ms)")
     ctx.close()
     del ctx
     torch.cuda.empty_cache()
@@ -171,7 +178,10 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-micro", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--prof-steps", type=int, default=5)
+    ap.add_argument("--prof-steps", type=int, default=50)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="first run one plain copy kernel of this many MiB (read and written once "
+                         "each), the reference dispatch for HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build runs all k learners on a single MI355X "
@@ -182,6 +192,16 @@ def main():
     import workloads as wl
 
     torch.cuda.set_device(0)
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)  # one elementwise kernel: n floats in, n floats out
+        torch.cuda.synchronize()
+        log(f"[bench] copy kernel: {n * 4} bytes read, {n * 4} bytes written")
+        del src, dst
+        torch.cuda.empty_cache()
     wk = wl.RESNET32_K4
     log(f"[bench] {wk.name}: warmup {args.warmup}, steps {args.steps}")
     ms, wall, loss, prof = time_training(wk, args.steps, args.warmup, prof_steps=args.prof_steps)

@@ -40,6 +40,7 @@ struct Op {
   bool bias = false, relu = false, need_dx = true;
   int64_t w_off = -1, b_off = -1;   // parameter offsets (elements)
   int splits = 1, chunk = 0;
+  int64_t part_off = -1;            // this layer's weight-gradient split partials
   bool emit_stats = false;          // epilogue writes BN partial sums
   int bnb = -1;                     // data-gradient epilogue feeds this BN's backward sums
   // batch norm
@@ -74,7 +75,7 @@ struct Plan {
   int input = -1, logits = -1;
   // workspace layout (bytes)
   int64_t off_W = 0, off_G = 0, off_Z = 0, off_Zp = 0, off_Wprev = -1;
-  int64_t off_loss = 0, off_flag = 0, off_bnpart = 0, off_split = 0;
+  int64_t off_loss = 0, off_flag = 0, off_bnpart = 0;
   int64_t total = 0;
 };
 
@@ -374,15 +375,16 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p) {
       }
     }
   }
-  int64_t bnpart = 0, split = 0;
+  int64_t bnpart = 0;
   for (size_t i = 0; i < p.ops.size(); ++i) {
     Op& o = p.ops[i];
     if (o.kind == OP_CONV) {
       if (!conv_supported(o.R, o.R, o.st, o.need_dx)) return false;
       ConvGeom g = geom(p, o);
       o.splits = conv_bwd_weight_splits(g, &o.chunk);
-      if (o.splits > 1)
-        split = std::max<int64_t>(split, (int64_t)k * o.splits * o.Co * o.Ci * o.R * o.R * 4);
+      // every layer keeps its own partials: one launch reduces them all
+      // after the backward pass
+      if (o.splits > 1) o.part_off = take((int64_t)k * o.splits * o.Co * o.Ci * o.R * o.R * 4);
     } else if (o.kind == OP_BN) {
       o.mean = take((int64_t)k * o.C * 4);
       o.istd = take((int64_t)k * o.C * 4);
@@ -401,7 +403,6 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p) {
   for (Op& o : p.ops)
     if (o.kind == OP_CONV && o.add_mode != ADD_NONE) o.add_buf = p.ops[o.add_buf].dres;
   p.off_bnpart = take(std::max<int64_t>(bnpart, 16));
-  p.off_split = take(std::max<int64_t>(split, 16));
   p.off_loss = take((int64_t)k * 4);
   p.off_flag = take(16);
   p.total = off;
@@ -435,13 +436,16 @@ struct cb_ctx {
   std::vector<ProfRec> recs;
   std::vector<hipEvent_t> evpool;
   std::vector<ProfAgg> agg;
+  // weight-gradient split reductions of all layers, one launch per table
+  std::vector<SplitTable> split_tables;
+  std::vector<double> split_bytes;
 
   ~cb_ctx() {
     for (auto& r : recs) {
-      hipEventDestroy(r.a);
-      hipEventDestroy(r.b);
+      (void)hipEventDestroy(r.a);
+      (void)hipEventDestroy(r.b);
     }
-    for (auto e : evpool) hipEventDestroy(e);
+    for (auto e : evpool) (void)hipEventDestroy(e);
   }
 
   template <class T>
@@ -481,22 +485,42 @@ hipEvent_t prof_event(cb_ctx* c) {
   return e;
 }
 
-// Brackets one launch with events when instrumentation is on.
+// Times the one kernel launch made inside the scope when instrumentation is
+// on: the events ride on that kernel's dispatch (see klaunch).
 struct ProfScope {
   cb_ctx* c;
-  hipEvent_t a = nullptr;
+  hipEvent_t a = nullptr, b = nullptr;
   explicit ProfScope(cb_ctx* cc) : c(cc) {
-    if (c->prof && (a = prof_event(c))) hipEventRecord(a, c->stream);
+    if (!c->prof) return;
+    a = prof_event(c);
+    b = a ? prof_event(c) : nullptr;
+    if (a && b) {
+      g_launch_timing.start = a;
+      g_launch_timing.stop = b;
+    }
   }
   void done(const char* name, double flops, double bytes) {
-    if (!c->prof || !a) return;
-    hipEvent_t b = prof_event(c);
-    if (!b) return;
-    hipEventRecord(b, c->stream);
-    c->recs.push_back(ProfRec{a, b, name, flops, bytes});
+    if (!a || !b) return;
+    if (g_launch_timing.start == a) {  // nothing was launched: give the events back
+      g_launch_timing = LaunchTiming();
+      c->evpool.push_back(a);
+      c->evpool.push_back(b);
+    } else {
+      c->recs.push_back(ProfRec{a, b, name, flops, bytes});
+    }
+    a = b = nullptr;
+  }
+  ~ProfScope() {
+    if (a && b && g_launch_timing.start == a) g_launch_timing = LaunchTiming();
+    if (a && b) {
+      c->evpool.push_back(a);
+      c->evpool.push_back(b);
+    }
   }
 };
 
+// One instrumented launch; `call` may overwrite nm_ with the name of the
+// kernel variant it launched.
 #define CB_LAUNCH(c, name, flops, bytes, call) \
   do {                                         \
     ProfScope ps_(c);                          \
@@ -559,7 +583,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         const double res = a.res_mode == RES_SAME ? n
                            : a.res_mode == RES_SUBSAMPLE ? (double)N * a.res_C * o.H * o.W : 0.0;
         if (o.parts == 0) CB_LAUNCH(c, "bn_stats_k", 0.0, 4.0 * n, bn_fwd_stats(a, s));
-        CB_LAUNCH(c, "bn_apply_k", 0.0, 4.0 * (2.0 * n + res), bn_fwd_apply(a, s));
+        CB_LAUNCH(c, "bn_apply_k", 0.0, 4.0 * (2.0 * n + res), bn_fwd_apply(a, s, &nm_));
         break;
       }
       case OP_MAXPOOL:
@@ -614,7 +638,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         const double mask = o.relu ? 1.0 : 0.0, dres = o.res >= 0 ? 1.0 : 0.0;
         if (o.bwd_parts == 0)
           CB_LAUNCH(c, "bn_bwd_stats_k", 0.0, 4.0 * n * (2.0 + mask), bn_bwd_stats(a, s));
-        CB_LAUNCH(c, "bn_bwd_apply_k", 0.0, 4.0 * n * (3.0 + mask + dres), bn_bwd_apply(a, s));
+        CB_LAUNCH(c, "bn_bwd_apply_k", 0.0, 4.0 * n * (3.0 + mask + dres), bn_bwd_apply(a, s, &nm_));
         break;
       }
       case OP_CONV: {
@@ -631,7 +655,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         w.dy = grd(o.out);
         w.dw = G + o.w_off;
         w.pstride = p.Pp;
-        w.partial = c->at<float>(p.off_split);
+        w.partial = o.splits > 1 ? c->at<float>(o.part_off) : nullptr;
         w.splits = o.splits;
         w.chunk = o.chunk;
         {
@@ -640,10 +664,6 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
           CB_HIP(c, conv_bwd_weight(w, s, &nm));
           ps.done(nm, flops, 4.0 * (xin + yout + k * wn));
         }
-        if (o.splits > 1)
-          CB_LAUNCH(c, "reduce_splits_k", 0.0, 4.0 * k * wn * (o.splits + 1.0),
-                    reduce_splits(w.partial, k, o.splits, (int64_t)o.Co * o.Ci * o.R * o.R,
-                                  G + o.w_off, p.Pp, s));
         if (o.need_dx) {
           ConvBwdDataArgs d;
           d.g = g;
@@ -676,6 +696,9 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
       }
     }
   }
+  for (size_t i = 0; i < c->split_tables.size(); ++i)
+    CB_LAUNCH(c, "reduce_splits_k", 0.0, c->split_bytes[i],
+              reduce_splits(c->split_tables[i], k, s));
   return CB_OK;
 }
 
@@ -781,6 +804,18 @@ int cb_create(const cb_model* m, int k, int b, float alpha, float lr, float mome
   }
   c->ws = static_cast<char*>(workspace_dev);
   c->stream = static_cast<hipStream_t>(hip_stream);
+  for (const Op& o : c->p.ops) {
+    if (o.kind != OP_CONV || o.splits <= 1) continue;
+    if (c->split_tables.empty() || c->split_tables.back().nseg == MAX_SPLIT_SEGS) {
+      c->split_tables.emplace_back();
+      c->split_tables.back().pstride = c->p.Pp;
+      c->split_bytes.push_back(0.0);
+    }
+    const int64_t wn = (int64_t)o.Co * o.Ci * o.R * o.R;
+    split_table_add(c->split_tables.back(), c->at<float>(o.part_off), c->G() + o.w_off, wn,
+                    o.splits);
+    c->split_bytes.back() += 4.0 * k * wn * (o.splits + 1.0);
+  }
   c->alpha = alpha;
   c->lr = lr;
   c->mu = momentum;

@@ -185,7 +185,8 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   }
 
   // epilogue: acc[t][u][i] is pixel (wave*TM + t)*16 + 4*kq + i, channel
-  // co0 + u*16 + (lane & 15) of this tile
+  // co0 + u*16 + (lane & 15) of this tile -- four consecutive pixels of one
+  // channel per lane, so every operand moves as one 16-byte access
   float* OUT = a.out + (int64_t)n_img * a.Cout * HW;
   double s1[TN], s2[TN];
 #pragma unroll
@@ -200,39 +201,56 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       bi = a.bn_istd[j * a.Cout + co];
     }
 #pragma unroll
-    for (int t = 0; t < TM; ++t)
+    for (int t = 0; t < TM; ++t) {
+      const int p0 = oh0 * WW + (wave * TM + t) * 16 + 4 * kq;  // first pixel in the plane
+      const int64_t idx = (int64_t)co * HW + p0;
+      v4f v = acc[t][u];
+      if (!FLIP) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int p = oh0 * WW + (wave * TM + t) * 16 + 4 * kq + i;  // pixel in the plane
-        const int64_t idx = (int64_t)co * HW + p;
-        float v = acc[t][u][i];
-        if (!FLIP) {
-          v += bv;
-          if (a.relu) v = v > 0.f ? v : 0.f;
-          OUT[idx] = v;
-          s1[u] += (double)v;
-          s2[u] += (double)v * v;
-        } else {
-          const int64_t gidx = (int64_t)n_img * a.Cout * HW + idx;
-          if (a.accumulate) v += OUT[idx];
-          if (a.add_mode == ADD_SAME) {
-            v += a.add[gidx];
-          } else if (a.add_mode == ADD_SUBSAMPLE) {
-            const int ih = p / WW, iw = p - ih * WW, st = a.add_st;
+        for (int i = 0; i < 4; ++i) {
+          float e = v[i] + bv;
+          if (a.relu) e = e > 0.f ? e : 0.f;
+          v[i] = e;
+          s1[u] += (double)e;
+          s2[u] += (double)e * e;
+        }
+        *reinterpret_cast<v4f*>(OUT + idx) = v;
+      } else {
+        const int64_t gidx = (int64_t)n_img * a.Cout * HW + idx;
+        if (a.accumulate) v += *reinterpret_cast<const v4f*>(OUT + idx);
+        if (a.add_mode == ADD_SAME) {
+          v += *reinterpret_cast<const v4f*>(a.add + gidx);
+        } else if (a.add_mode == ADD_SUBSAMPLE) {
+          const int st = a.add_st;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int p = p0 + i, ih = p / WW, iw = p - ih * WW;
             if (ih % st == 0 && iw % st == 0)
-              v += a.add[(((int64_t)n_img * a.add_C + co) * (H / st) + ih / st) * (WW / st) +
-                         iw / st];
+              v[i] += a.add[(((int64_t)n_img * a.add_C + co) * (H / st) + ih / st) * (WW / st) +
+                            iw / st];
           }
-          if (a.mask && !(a.mask[gidx] > 0.f)) v = 0.f;
-          OUT[idx] = v;
-          if (a.bn_part) {
-            const float d = (a.bn_y && !(a.bn_y[gidx] > 0.f)) ? 0.f : v;
-            const float xh = (a.bn_x[gidx] - bm) * bi;
+        }
+        if (a.mask) {
+          const v4f m = *reinterpret_cast<const v4f*>(a.mask + gidx);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (!(m[i] > 0.f)) v[i] = 0.f;
+        }
+        *reinterpret_cast<v4f*>(OUT + idx) = v;
+        if (a.bn_part) {
+          const v4f xv = *reinterpret_cast<const v4f*>(a.bn_x + gidx);
+          v4f yv = v4f{1.f, 1.f, 1.f, 1.f};
+          if (a.bn_y) yv = *reinterpret_cast<const v4f*>(a.bn_y + gidx);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float d = (yv[i] > 0.f) ? v[i] : 0.f;
+            const float xh = (xv[i] - bm) * bi;
             s1[u] += (double)d;
             s2[u] += (double)d * xh;
           }
         }
       }
+    }
   }
   double* part = FLIP ? a.bn_part : a.stats;
   if (!part) return;
@@ -261,6 +279,154 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   }
 }
 
+// Weight gradient of the same convolutions:
+//   dW[co][ci][r][s] = sum over the replica's images n and pixels p of
+//                      dY[n][co][p] * X[n][ci][p + (r - 1, s - 1)].
+// A workgroup owns one 16 x 16 block of (co, ci) and all nine taps, and a
+// run of "units" (TH full rows of one image).  Per unit it stages dY
+// [16][TH*WW] and the X rows with their halo [16][TH+2][WW+2] in LDS once;
+// every tap then reads X at a constant offset.  MFMA: rows = co (A = dY),
+// columns = ci (B = X), contraction = 4 consecutive pixels of one row.  The
+// four waves take interleaved 4-pixel steps and their partial sums are
+// added in wave order; the result goes to dw (one split) or to the split's
+// slot of `partial` for the fixed-order split reduction.
+struct WgradArgs {
+  int k, b, H;
+  int Ci, Co;
+  const float* x;   // [k*b][Ci][H][W]
+  const float* dy;  // [k*b][Co][H][W]
+  float* dw;        // replica 0 gradient [Co][Ci][3][3] (splits == 1)
+  int64_t pstride;
+  float* partial;   // [k][splits][Co][Ci*9] (splits > 1)
+  int splits, per;  // units of a replica: b * H / TH, `per` of them per split
+};
+
+// LDS row stride with stride % 64 == 34: the 16 channels x 4 pixels a
+// 64-lane read touches fall on (nearly) distinct banks.
+constexpr int pad34(int n) { return n + ((34 - n % 64) + 64) % 64; }
+
+template <int WW, int TH>
+__global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
+  constexpr int WP = WW + 2, HR = TH + 2;
+  constexpr int SA = pad34(TH * WW);      // dY tile channel stride
+  constexpr int SB = pad34(HR * WP);      // X tile channel stride
+  constexpr int NQ = TH * WW / 4;         // 4-pixel steps per unit
+  constexpr int QW = NQ / 4;              // per wave
+  constexpr int NA4 = 16 * TH * WW / 4;   // dY float4s per unit
+  constexpr int NA4T = (NA4 + 255) / 256;
+  constexpr int NX = 16 * HR * WP;        // X elements per unit
+  constexpr int NXT = (NX + 255) / 256;
+  constexpr int RED = 4 * 16 * 144;       // cross-wave reduction buffer
+  constexpr int TILE = 16 * SA + 16 * SB;
+  static_assert(NQ % 4 == 0, "unit must split evenly over the waves");
+  __shared__ __attribute__((aligned(16))) float lds[TILE > RED ? TILE : RED];
+  float* As = lds;
+  float* Bs = lds + 16 * SA;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4, l16 = lane & 15;
+  const int nci = a.Ci / 16;
+  const int co0 = (blockIdx.x / nci) * 16, ci0 = (blockIdx.x % nci) * 16;
+  const int split = blockIdx.y, j = blockIdx.z;
+  const int H = a.H, HW = H * WW, tiles_img = H / TH;
+  const int units = a.b * tiles_img;
+  const int u0 = split * a.per, u1 = min(units, u0 + a.per);
+
+  v4f acc[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  for (int u = u0; u < u1; ++u) {
+    const int img = u / tiles_img, h0 = (u - img * tiles_img) * TH;
+    const int n = j * a.b + img;
+    const float* DY = a.dy + ((int64_t)n * a.Co + co0) * HW + h0 * WW;
+    const float* X = a.x + ((int64_t)n * a.Ci + ci0) * HW;
+    v4f ra[NA4T];
+    float rx[NXT];
+#pragma unroll
+    for (int i = 0; i < NA4T; ++i) {
+      const int e = tid + i * 256;
+      if (e < NA4) {
+        const int c = e / (TH * WW / 4), q = e - c * (TH * WW / 4);
+        ra[i] = *reinterpret_cast<const v4f*>(DY + (int64_t)c * HW + q * 4);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NXT; ++i) {
+      const int e = tid + i * 256;
+      float v = 0.f;
+      if (e < NX) {
+        const int c = e / (HR * WP), rem = e - c * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
+        const int ih = h0 - 1 + hr, iw = wc - 1;
+        if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)WW)
+          v = X[(int64_t)c * HW + ih * WW + iw];
+      }
+      rx[i] = v;
+    }
+    __syncthreads();  // the previous unit's reads of the tiles are done
+#pragma unroll
+    for (int i = 0; i < NA4T; ++i) {
+      const int e = tid + i * 256;
+      if (e < NA4) {
+        const int c = e / (TH * WW / 4), q = e - c * (TH * WW / 4);
+        float* d = As + c * SA + q * 4;
+        d[0] = ra[i][0];
+        d[1] = ra[i][1];
+        d[2] = ra[i][2];
+        d[3] = ra[i][3];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NXT; ++i) {
+      const int e = tid + i * 256;
+      if (e < NX) {
+        const int c = e / (HR * WP), rem = e - c * (HR * WP);
+        Bs[c * SB + rem] = rx[i];
+      }
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int i = 0; i < QW; ++i) {
+      const int q = wave + 4 * i;
+      const int h = q / (WW / 4), w = (q - h * (WW / 4)) * 4;
+      const float av = As[l16 * SA + h * WW + w + kq];
+      const float* xb = Bs + l16 * SB + h * WP + w + kq;
+      float bv[9];
+#pragma unroll
+      for (int t = 0; t < 9; ++t) bv[t] = xb[(t / 3) * WP + (t % 3)];
+#pragma unroll
+      for (int t = 0; t < 9; ++t) acc[t] = mfma4(av, bv[t], acc[t]);
+    }
+  }
+
+  // acc[t][r]: co = co0 + 4*kq + r, ci = ci0 + l16, tap t.  Waves in order.
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) lds[(wave * 16 + 4 * kq + r) * 144 + l16 * 9 + t] = acc[t][r];
+  __syncthreads();
+  const int64_t wn = (int64_t)a.Co * a.Ci * 9;
+  float* out = a.splits == 1 ? a.dw + (int64_t)j * a.pstride
+                             : a.partial + (int64_t)(j * a.splits + split) * wn;
+  for (int e = tid; e < 16 * 144; e += 256) {
+    const int c = e / 144, rem = e - c * 144;
+    const float v = ((lds[e] + lds[2304 + e]) + lds[4608 + e]) + lds[6912 + e];
+    out[(int64_t)(co0 + c) * a.Ci * 9 + ci0 * 9 + rem] = v;
+  }
+}
+
+template <int WW, int TH>
+hipError_t launch_wgrad(const WgradArgs& a, hipStream_t s, const char** name) {
+  dim3 grid((unsigned)((a.Co / 16) * (a.Ci / 16)), (unsigned)a.splits, (unsigned)a.k);
+  klaunch(conv3x3_wgrad_k<WW, TH>, grid, dim3(256), 0, s, a);
+  if (name) {
+    static const std::string n =
+        std::string("conv3x3_wgrad_k<") + std::to_string(WW) + ", " + std::to_string(TH) + ">";
+    *name = n.c_str();
+  }
+  return hipGetLastError();
+}
+
 template <int WW, int TH, int BN, int CC, bool FLIP>
 const char* direct_name() {
   static const std::string n = std::string("conv3x3_k<") + std::to_string(WW) + ", " +
@@ -272,7 +438,7 @@ const char* direct_name() {
 template <int WW, int TH, int BN, int CC, bool FLIP>
 hipError_t launch(const DirectArgs& a, hipStream_t s, const char** name) {
   dim3 grid((unsigned)(a.b * (a.H / TH)), (unsigned)(a.Cout / BN), (unsigned)a.k);
-  hipLaunchKernelGGL((conv3x3_k<WW, TH, BN, CC, FLIP>), grid, dim3(256), 0, s, a);
+  klaunch((conv3x3_k<WW, TH, BN, CC, FLIP>), grid, dim3(256), 0, s, a);
   if (name) *name = direct_name<WW, TH, BN, CC, FLIP>();
   return hipGetLastError();
 }
@@ -321,7 +487,42 @@ hipError_t dispatch(const DirectArgs& a, int W, hipStream_t s, const char** name
   return dispatch_w<FLIP, 8>(a, t, s, name);
 }
 
+// Weight gradient: units of 8 rows; the split gives every CU two
+// workgroups over all replicas and channel blocks where the units allow.
+constexpr int WG_TH = 8;
+
+void wgrad_split(const ConvGeom& g, int* splits, int* per) {
+  const int units = g.b * (g.H / WG_TH);
+  const int64_t blocks = (int64_t)g.k * (g.Co / 16) * (g.Ci / 16);
+  int sp = (int)std::max<int64_t>(1, std::min<int64_t>(units, (DIRECT_MIN_WGS + blocks - 1) / blocks));
+  const int pr = (units + sp - 1) / sp;
+  *per = pr;
+  *splits = (units + pr - 1) / pr;
+}
+
 }  // namespace
+
+bool conv_direct_wgrad_ok(const ConvGeom& g) {
+  return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad);
+}
+
+int conv_direct_wgrad_splits(const ConvGeom& g) {
+  int sp = 1, per = 1;
+  wgrad_split(g, &sp, &per);
+  return sp;
+}
+
+hipError_t conv_direct_wgrad(const ConvBwdWeightArgs& w, hipStream_t s, const char** name) {
+  WgradArgs a{};
+  a.k = w.g.k; a.b = w.g.b; a.H = w.g.H;
+  a.Ci = w.g.Ci; a.Co = w.g.Co;
+  a.x = w.x; a.dy = w.dy; a.dw = w.dw; a.pstride = w.pstride; a.partial = w.partial;
+  wgrad_split(w.g, &a.splits, &a.per);
+  if (w.splits != a.splits) return hipErrorInvalidValue;  // scratch sized for another split
+  if (w.g.W == 32) return launch_wgrad<32, WG_TH>(a, s, name);
+  if (w.g.W == 16) return launch_wgrad<16, WG_TH>(a, s, name);
+  return launch_wgrad<8, WG_TH>(a, s, name);
+}
 
 bool conv_direct_fwd_ok(const ConvGeom& g) {
   return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad);

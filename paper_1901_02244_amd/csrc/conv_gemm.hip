@@ -524,24 +524,44 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
     }
 }
 
-// dw[j][e] = sum over s of part[j][s][e], s in order.  A block covers 64
-// elements; its 4 waves take the splits in 4 contiguous runs, combined in
-// run order.
-__global__ __launch_bounds__(256) void reduce_splits_k(const float* part, int splits, int64_t n,
-                                                       float* dw, int64_t pstride) {
+// Split reduction of several layers in one launch:
+//   dw[j][e] = sum over s of partial[j][s][e], s in order,
+// for every segment of the table.  A block covers 64 elements of one
+// segment and one replica; its 4 waves take the splits in 4 contiguous
+// runs (loads U at a time, adds in order), combined in run order.
+__global__ __launch_bounds__(256) void reduce_splits_k(SplitTable t) {
   __shared__ float red[4][64];
-  const int j = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t e = (int64_t)blockIdx.x * 64 + lane;
+  const int bx = blockIdx.x, j = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int lo = 0, hi = t.nseg - 1;  // the last segment whose first block is <= bx
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (t.seg[mid].block0 <= bx) lo = mid;
+    else hi = mid - 1;
+  }
+  const float* part = t.seg[lo].partial;
+  float* dw = t.seg[lo].dw;
+  const int64_t n = t.seg[lo].n;
+  const int splits = t.seg[lo].splits;
+  const int64_t e = (int64_t)(bx - t.seg[lo].block0) * 64 + lane;
   const int per = (splits + 3) / 4, s0 = w * per, s1 = min(splits, s0 + per);
   float s = 0.f;
   if (e < n) {
     const float* p = part + (int64_t)j * splits * n + e;
-    for (int i = s0; i < s1; ++i) s += p[(int64_t)i * n];
+    constexpr int U = 8;
+    int i = s0;
+    for (; i + U <= s1; i += U) {
+      float v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = p[(int64_t)(i + u) * n];
+#pragma unroll
+      for (int u = 0; u < U; ++u) s += v[u];
+    }
+    for (; i < s1; ++i) s += p[(int64_t)i * n];
   }
   red[w][lane] = s;
   __syncthreads();
   if (w == 0 && e < n)
-    dw[(int64_t)j * pstride + e] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+    dw[(int64_t)j * t.pstride + e] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -590,7 +610,7 @@ hipError_t launch_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
   constexpr int BK = stage_k<BM>();
   const int M = a.g.b * a.g.Ho * a.g.Wo;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Co, BN), a.g.k);
-  hipLaunchKernelGGL((conv_fwd_k<BM, BN, WM, WN, R, BK>), grid, dim3(256), 0, s, a);
+  klaunch((conv_fwd_k<BM, BN, WM, WN, R, BK>), grid, dim3(256), 0, s, a);
   if (name) *name = tile_name<0, BM, BN, WM, WN, R, 0, BK>();
   return hipGetLastError();
 }
@@ -600,7 +620,7 @@ hipError_t launch_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char**
   constexpr int BK = stage_k<BM>();
   const int M = a.g.b * a.g.H * a.g.W;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Ci, BN), a.g.k);
-  hipLaunchKernelGGL((conv_bwd_data_k<BM, BN, WM, WN, R, ST, BK>), grid, dim3(256), 0, s, a);
+  klaunch((conv_bwd_data_k<BM, BN, WM, WN, R, ST, BK>), grid, dim3(256), 0, s, a);
   if (name) *name = tile_name<1, BM, BN, WM, WN, R, ST, BK>();
   return hipGetLastError();
 }
@@ -610,7 +630,7 @@ constexpr int WG_BK = 32;  // pixels per stage of the weight gradient
 template <int BM, int BN, int WM, int WN, int R>
 hipError_t launch_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char** name) {
   dim3 grid(cdiv(a.g.Co, BM), cdiv(a.g.Ci * R * R, BN), a.g.k * a.splits);
-  hipLaunchKernelGGL((conv_bwd_weight_k<BM, BN, WM, WN, R, WG_BK>), grid, dim3(256), 0, s, a);
+  klaunch((conv_bwd_weight_k<BM, BN, WM, WN, R, WG_BK>), grid, dim3(256), 0, s, a);
   if (name) *name = tile_name<2, BM, BN, WM, WN, R, 0, WG_BK>();
   return hipGetLastError();
 }
@@ -671,6 +691,8 @@ hipError_t bwd_weight_r(const ConvBwdWeightArgs& a, hipStream_t s, const char** 
 
 }  // namespace
 
+inline bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 int conv_fwd_tiles_m(const ConvGeom& g) {
   if (conv_direct_fwd_ok(g)) return conv_direct_fwd_tiles(g);
   const int64_t M = (int64_t)g.b * g.Ho * g.Wo;
@@ -684,6 +706,10 @@ int conv_bwd_data_tiles_m(const ConvGeom& g) {
 }
 
 int conv_bwd_weight_splits(const ConvGeom& g, int* chunk) {
+  if (conv_direct_wgrad_ok(g)) {
+    *chunk = 0;
+    return conv_direct_wgrad_splits(g);
+  }
   const int L = g.b * g.Ho * g.Wo;
   const int bm = bwd_weight_bm(g.Co);
   const int64_t tiles = (int64_t)cdiv(g.Co, bm) * cdiv(g.Ci * g.R * g.S, 64) * g.k;
@@ -703,7 +729,9 @@ bool conv_supported(int R, int S, int st, bool need_dx) {
 }
 
 hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
-  if (conv_direct_fwd_ok(a.g)) return conv_direct_fwd(a, s, name);
+  // the direct kernel moves its outputs in 16-byte pieces (workspace
+  // tensors are 256-byte aligned, so layers of a plan always qualify)
+  if (conv_direct_fwd_ok(a.g) && al16(a.y)) return conv_direct_fwd(a, s, name);
   switch (a.g.R) {
     case 1: return fwd_r<1>(a, s, name);
     case 3: return fwd_r<3>(a, s, name);
@@ -714,7 +742,9 @@ hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
 }
 
 hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
-  if (conv_direct_bwd_data_ok(a.g)) return conv_direct_bwd_data(a, s, name);
+  if (conv_direct_bwd_data_ok(a.g) && al16(a.dx) && al16(a.mask) && al16(a.bn_x) &&
+      al16(a.bn_y) && (a.add_mode != ADD_SAME || al16(a.add)))
+    return conv_direct_bwd_data(a, s, name);
   const int key = a.g.R * 10 + a.g.st;
   switch (key) {
     case 11: return bwd_data_r<1, 1>(a, s, name);
@@ -727,6 +757,8 @@ hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** n
 }
 
 hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char** name) {
+  if (conv_direct_wgrad_ok(a.g))  // reads dY in 16-byte pieces
+    return al16(a.dy) ? conv_direct_wgrad(a, s, name) : hipErrorInvalidValue;
   switch (a.g.R) {
     case 1: return bwd_weight_r<1>(a, s, name);
     case 3: return bwd_weight_r<3>(a, s, name);
@@ -736,16 +768,25 @@ hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char
   }
 }
 
-hipError_t reduce_splits(const float* partial, int k, int splits, int64_t n, float* dw,
-                         int64_t pstride, hipStream_t s) {
-  hipLaunchKernelGGL(reduce_splits_k, dim3(cdiv(n, 64), k), dim3(256), 0, s, partial, splits, n,
-                     dw, pstride);
+hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s) {
+  if (t.nseg < 1 || t.nseg > MAX_SPLIT_SEGS) return hipErrorInvalidValue;
+  klaunch(reduce_splits_k, dim3(t.blocks, k), dim3(256), 0, s, t);
   return hipGetLastError();
+}
+
+void split_table_add(SplitTable& t, const float* partial, float* dw, int64_t n, int splits) {
+  SplitSeg& g = t.seg[t.nseg++];
+  g.partial = partial;
+  g.dw = dw;
+  g.n = n;
+  g.splits = splits;
+  g.block0 = t.blocks;
+  t.blocks += (int)cdiv(n, 64);
 }
 
 hipError_t channel_sum(const float* dy, int k, int b, int C, int HW, float* db, int64_t pstride,
                        hipStream_t s) {
-  hipLaunchKernelGGL(channel_sum_k, dim3(C, k), dim3(256), 0, s, dy, b, C, HW, db, pstride);
+  klaunch(channel_sum_k, dim3(C, k), dim3(256), 0, s, dy, b, C, HW, db, pstride);
   return hipGetLastError();
 }
 

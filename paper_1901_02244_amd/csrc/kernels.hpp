@@ -5,10 +5,29 @@
 // params + j*pstride.  Every launcher enqueues on the given stream and
 // returns the hipError_t of the launch.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace cbk {
+
+// Per-launch timing.  When armed, the next kernel launch on this thread
+// passes the two events to hipExtLaunchKernel, which stamps them on the
+// kernel's own dispatch: the interval is the kernel alone, with no marker
+// packets added around it.  Every kernel of this library goes through
+// klaunch.
+struct LaunchTiming {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+inline thread_local LaunchTiming g_launch_timing;
+
+template <typename... P, typename... A>
+inline void klaunch(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t shm, hipStream_t s,
+                    A... args) {
+  const LaunchTiming t = g_launch_timing;
+  g_launch_timing = LaunchTiming();
+  hipExtLaunchKernelGGL(kernel, grid, block, shm, s, t.start, t.stop, 0u, args...);
+}
 
 // Geometry of one convolution layer (an FC layer is a 1x1 conv on a 1x1
 // image).  b = images per replica, k = replicas.
@@ -97,12 +116,33 @@ bool conv_direct_fwd_ok(const ConvGeom& g);
 bool conv_direct_bwd_data_ok(const ConvGeom& g);
 int conv_direct_fwd_tiles(const ConvGeom& g);
 int conv_direct_bwd_data_tiles(const ConvGeom& g);
+// Their weight gradient has a direct kernel too (conv_bwd_weight routes;
+// conv_bwd_weight_splits reports its split).
+bool conv_direct_wgrad_ok(const ConvGeom& g);
+int conv_direct_wgrad_splits(const ConvGeom& g);
+hipError_t conv_direct_wgrad(const ConvBwdWeightArgs& a, hipStream_t s,
+                             const char** name = nullptr);
 hipError_t conv_direct_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name = nullptr);
 hipError_t conv_direct_bwd_data(const ConvBwdDataArgs& a, hipStream_t s,
                                 const char** name = nullptr);
-// dw[j][e] = sum over splits of partial[j][s][e], s in order.
-hipError_t reduce_splits(const float* partial, int k, int splits, int64_t n, float* dw,
-                         int64_t pstride, hipStream_t s);
+// Weight-gradient split reduction of up to MAX_SPLIT_SEGS layers in one
+// launch (the table travels as the kernel argument):
+//   seg.dw[j*pstride + e] = sum over s of seg.partial[j][s][e], s in order.
+constexpr int MAX_SPLIT_SEGS = 80;
+struct SplitSeg {
+  const float* partial;  // [k][splits][n]
+  float* dw;             // replica 0 destination
+  int64_t n;
+  int splits;
+  int block0;            // first 64-element block of this segment
+};
+struct SplitTable {
+  int nseg = 0, blocks = 0;
+  int64_t pstride = 0;
+  SplitSeg seg[MAX_SPLIT_SEGS];
+};
+void split_table_add(SplitTable& t, const float* partial, float* dw, int64_t n, int splits);
+hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s);
 // db[j][c] = sum over replica j's images and pixels of dy[n][c][p].
 hipError_t channel_sum(const float* dy, int k, int b, int C, int HW, float* db,
                        int64_t pstride, hipStream_t s);
@@ -147,12 +187,12 @@ int bn_chunks(int b, int HW, int C, int k);
 // Forward: per-chunk fp64 sums (parts = chunks), then normalise (+ residual,
 // ReLU).  The sums can instead come from the producing conv's epilogue.
 hipError_t bn_fwd_stats(const BNArgs& a, hipStream_t s);
-hipError_t bn_fwd_apply(const BNArgs& a, hipStream_t s);
+hipError_t bn_fwd_apply(const BNArgs& a, hipStream_t s, const char** name = nullptr);
 // Backward: per-chunk fp64 sums of dy and dy*xhat (parts = chunks), then dx
 // and dgamma/dbeta.  The sums can instead come from the epilogue of the
 // data-gradient GEMM that wrote dy.
 hipError_t bn_bwd_stats(const BNBwdArgs& a, hipStream_t s);
-hipError_t bn_bwd_apply(const BNBwdArgs& a, hipStream_t s);
+hipError_t bn_bwd_apply(const BNBwdArgs& a, hipStream_t s, const char** name = nullptr);
 
 hipError_t maxpool_fwd(const float* x, int N, int C, int H, int W, int K, int st, int pad,
                        float* y, int Ho, int Wo, int* arg, hipStream_t s);

@@ -114,7 +114,7 @@ hipError_t launch_r(const SMAArgs& a, bool nt, hipStream_t s) {
   dim3 grid(cdiv(a.P4, 4 * C)), block(256);
   const bool lm = a.Wprev != nullptr;
 #define CB_SMA_LAUNCH(CORR, LM, NTV) \
-  hipLaunchKernelGGL((sma_k<R, CORR, LM, NTV>), grid, block, 0, s, a)
+  klaunch((sma_k<R, CORR, LM, NTV>), grid, block, 0, s, a)
   if (a.correct) {
     if (lm) {
       if (nt) CB_SMA_LAUNCH(true, true, true); else CB_SMA_LAUNCH(true, true, false);
@@ -162,12 +162,12 @@ hipError_t sma_step(const SMAArgs& a, hipStream_t s) {
 }
 
 hipError_t nonfinite_scan(const float* z, int64_t n, int* flag, hipStream_t s) {
-  hipLaunchKernelGGL(nonfinite_k, dim3(cdiv(n, 256)), dim3(256), 0, s, z, n, flag);
+  klaunch(nonfinite_k, dim3(cdiv(n, 256)), dim3(256), 0, s, z, n, flag);
   return hipGetLastError();
 }
 
 hipError_t zero_ints(int* p, int n, hipStream_t s) {
-  hipLaunchKernelGGL(zero_ints_k, dim3(cdiv(n, 256)), dim3(256), 0, s, p, n);
+  klaunch(zero_ints_k, dim3(cdiv(n, 256)), dim3(256), 0, s, p, n);
   return hipGetLastError();
 }
 

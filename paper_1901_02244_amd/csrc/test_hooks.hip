@@ -83,7 +83,12 @@ int cb_test_conv(int k, int b, int Ci, int H, int W, int Co, int R, int stride, 
   w.splits = conv_bwd_weight_splits(g, &w.chunk);
   rc = rc_of(conv_bwd_weight(w, s));
   if (rc) return rc;
-  if (w.splits > 1) rc = rc_of(reduce_splits(w.partial, k, w.splits, nw, grads, pstride, s));
+  if (w.splits > 1) {
+    SplitTable t;
+    t.pstride = pstride;
+    split_table_add(t, w.partial, grads, nw, w.splits);
+    rc = rc_of(reduce_splits(t, k, s));
+  }
   if (rc || !dx) return rc;
   ConvBwdDataArgs d;
   d.g = g;

@@ -237,6 +237,27 @@ def test_resnet32_k4_b32_full_size_learners():
         assert err <= tol, (j, err, where, "margin", margin)
 
 
+def test_resnet32_k4_b32_hundred_iterations():
+    """The full ResNet-32 workload (k = 4 learners of 32 images) for 100 SMA
+    iterations against the oracle's stored central model after the same 100
+    iterations (tests/golden/make_golden.py resnet32_z100).  The bound is
+    the larger of 1e-3 and twice the oracle's own drift at step 100 when w0
+    moves by one part in 1e7 (resnet32_envelope)."""
+    wk = wl.RESNET32_K4
+    env = json.load(open(os.path.join(GOLDEN, "resnet32_k4_b32_envelope.json")))["rel_l2"]
+    meta = json.load(open(os.path.join(GOLDEN, "resnet32_k4_b32_z100.json")))
+    z100 = np.load(os.path.join(GOLDEN, meta["file"]))
+    m = cb.model("resnet32", wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
+    layout = cb.cb_tensor_layout(m)
+    ctx = cb.Context(m, wk.k, wk.b, wk.alpha, wk.lr, wk.momentum, wl.init_w0(layout, wk.seed))
+    for t in range(100):
+        x, y = wl.workload_batch(wk, t)
+        ctx.cb_step(_dev(x), _dev(y))
+        ctx.cb_sync()
+    err = rel_l2(ctx.cb_get_central(), z100)
+    assert err <= max(TOL_Z_L2, 2 * env["100"]), (err, env["100"])
+
+
 def test_resnet50_k2_b32_full_size_learner0():
     """Full-size ResNet-50 workload (k = 2 learners of 32 images, 224x224):
     learner 0's loss and sampled gradient entries against the oracle's
