@@ -12,6 +12,7 @@ python bench.py [--gpus 1] [--steps K] [--warmup W]
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -40,22 +41,52 @@ def _ring(wk, n, dev):
     return xs, ys
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_resnet32_k4_b32.json")
+
+
+def kernel_source_hash():
+    """sha256 over the HIP sources the kernels are built from."""
+    csrc = os.path.join(ROOT, "paper_1901_02244_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".hpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy kernel), or
+    None when the summary is missing, covers no such kernel, or was taken
+    on other kernel sources."""
+    try:
+        doc = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if doc.get("source_sha256") != kernel_source_hash():
+        return None
+    k = doc.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return round(k["fetch_bytes_per_launch"] + k["write_bytes_per_launch"])
+
+
 def roofline_of(prof):
     """Roofline object for the kernel with the largest total time in a
-    profile {name: (launches, ms, flops, bytes)}."""
+    profile {name: (launches, ms, flops, bytes)}: algorithmic work per
+    launch over the average launch duration."""
     name, (la, ms, fl, by) = max(prof.items(), key=lambda kv: kv[1][1])
+    base = {"kernel": name, "launches_per_step": la, "avg_launch_us": round(ms * 1e3 / la, 3),
+            "traffic": measured_traffic(name), "algorithmic_bytes_per_launch": round(by / la)}
     if fl > 0:
         ach = fl / (ms * 1e-3) / 1e12
-        return {"kernel": name, "bound": "mfma", "achieved": round(ach, 3),
-                "peak": FP32_MFMA_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": round(ach / FP32_MFMA_PEAK_TFS, 4), "traffic": None,
-                "launches": la, "avg_launch_us": round(ms * 1e3 / la, 2),
-                "algorithmic_per_launch": fl / la}
+        return {"bound": "mfma", "achieved": round(ach, 3), "peak": FP32_MFMA_PEAK_TFS,
+                "unit": "TFLOP/s", "frac": round(ach / FP32_MFMA_PEAK_TFS, 4), **base,
+                "algorithmic_flops_per_launch": round(fl / la)}
     ach = by / (ms * 1e-3) / 1e9
-    return {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
-            "launches": la, "avg_launch_us": round(ms * 1e3 / la, 2),
-            "algorithmic_per_launch": by / la}
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBS, 4), **base}
 
 
 def time_training(wk, steps, warmup, ring=8, prof_steps=0):
@@ -144,41 +175,76 @@ def sma_micro(steps=20, warmup=3):
     del ctx, g
     torch.cuda.empty_cache()
     la, kms, _, kby = prof["sma_k"]
+    # a plain copy of the same size on the same box, for scale
+    half = nbytes // 8
+    src = torch.empty(half, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * half * 4 / (c0.elapsed_time(c1) / 5) / 1e6
+    del src, dst
+    torch.cuda.empty_cache()
     return {"P": P, "k": k, "ms": round(ms, 4), "bytes": nbytes,
+            "copy_GB/s": round(copy_gbs, 1), "frac_of_copy": round(nbytes / ms / 1e6 / copy_gbs, 4),
             "GB/s": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4),
             "kernel_avg_us": round(kms * 1e3 / la, 2),
             "kernel_GB/s": round(kby / (kms * 1e-3) / 1e9, 1),
             "kernel_frac_hbm": round(kby / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
 
 
-def cpu_baseline(wk):
-    """The oracle as it stands: one SMA iteration of the same workload on one core."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wk, iters=3):
+    """The oracle as it stands (single-threaded C), pinned to one host core:
+    `iters` SMA iterations of the same workload on the same inputs."""
     import oracle
     import workloads as wl
 
+    n_host = os.cpu_count()
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+    except (AttributeError, OSError):
+        pass
     m = oracle.model(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
     w0 = wl.init_w0(oracle.tensors(m), wk.seed)
     ref = oracle.SMA(m, w0, wk.k, wk.b, wk.alpha, wk.lr, wk.momentum)
-    x, y = wl.workload_batch(wk, 0)
     t0 = time.perf_counter()
-    ref.step(x, y)
-    ref.sync()
+    for t in range(iters):
+        x, y = wl.workload_batch(wk, t)
+        ref.step(x, y)
+        ref.sync()
     dt = time.perf_counter() - t0
-    return {"value": round(wk.n_images / dt, 3), "unit": "images/s", "cores": 1, "kind": "oracle",
-            "sample": f"1 SMA iteration of {wk.name} ({wk.n_images} images, all {wk.k} learners "
-                      f"+ sync), single-threaded, {dt:.1f} s"}
+    return {"value": round(iters * wk.n_images / dt, 3), "unit": "images/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{iters} SMA iterations of {wk.name} ({iters * wk.n_images} images, all "
+                      f"{wk.k} learners + sync) in {dt:.1f} s, single-threaded on 1 of {n_host} "
+                      f"host cores ({cpu_model()})"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--sweep-steps", type=int, default=20)
+    ap.add_argument("--sweep-steps", type=int, default=100)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-micro", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--prof-steps", type=int, default=50)
+    ap.add_argument("--prof-steps", type=int, default=100)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run one plain copy kernel of this many MiB (read and written once "
                          "each), the reference dispatch for HBM byte counters")
@@ -209,11 +275,17 @@ def main():
     log(f"[bench] {wk.name}: {ms:.3f} ms/step (wall {wall:.3f}), {value:.0f} images/s")
     roof = roofline_of(prof)
     tot = sum(v[1] for v in prof.values())
-    kernels = {k: {"launches_per_step": v[0], "ms_per_step": round(v[1], 4),
-                   "share": round(v[1] / tot, 4),
-                   "TFLOP/s": round(v[2] / (v[1] * 1e-3) / 1e12, 2) if v[2] else None,
-                   "GB/s": round(v[3] / (v[1] * 1e-3) / 1e9, 1)}
-               for k, v in sorted(prof.items(), key=lambda kv: -kv[1][1])}
+    def kernel_entry(v):
+        e = {"launches_per_step": v[0], "ms_per_step": round(v[1], 4), "share": round(v[1] / tot, 4),
+             "GB/s": round(v[3] / (v[1] * 1e-3) / 1e9, 1)}
+        if v[2]:  # a contraction: algorithmic fp32 MFMA utilisation
+            tf = v[2] / (v[1] * 1e-3) / 1e12
+            e.update({"TFLOP/s": round(tf, 2), "mfma_frac": round(tf / FP32_MFMA_PEAK_TFS, 4)})
+        else:
+            e["hbm_frac"] = round(v[3] / (v[1] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+        return e
+
+    kernels = {k: kernel_entry(v) for k, v in sorted(prof.items(), key=lambda kv: -kv[1][1])}
     for k_, v_ in kernels.items():
         log(f"[bench]   {k_}: {v_}")
     log(f"[bench] roofline: {roof}")
@@ -255,6 +327,7 @@ def main():
         "roofline": roof,
         "kernels_per_step": kernels,
         "k_sweep_b16": sweep,
+        "k_sweep_best": max(sweep, key=lambda k: sweep[k]["images_per_s"]) if sweep else None,
         "sma_microbench": micro,
         "cpu_baseline": cpu,
         "final_loss": [round(float(v), 4) for v in loss],

@@ -93,7 +93,8 @@ size_t cb_workspace_bytes(const cb_model* m, int k, int b);
  *   workspace_dev: at least cb_workspace_bytes(m, k, b) bytes, 256-byte
  *   aligned.  hip_stream: a hipStream_t (NULL = the default stream).
  * Blocks until w0 is on the device.  On success *out owns no device memory
- * of its own beyond the caller's workspace. */
+ * of its own beyond the caller's workspace; it does own a second HIP stream
+ * (default priority) and some events, released by cb_destroy. */
 int cb_create(const cb_model* m, int k, int b, float alpha, float lr, float momentum,
               const float* w0_host, int64_t n_params, void* workspace_dev, size_t ws_bytes,
               void* hip_stream, cb_ctx** out);
@@ -105,7 +106,10 @@ int cb_create(const cb_model* m, int k, int b, float alpha, float lr, float mome
  * never synchronised, its gradient is first applied as a local step without
  * correction (a sync interval above one).  inputs_dev / labels_dev must stay
  * unchanged until the work completes.  A label outside [0, classes) makes
- * that learner's loss NaN and contributes no one-hot term. */
+ * that learner's loss NaN and contributes no one-hot term.  The weight
+ * gradients run on the context's second stream, overlapping the rest of the
+ * backward pass; the step's last operation on the caller's stream waits for
+ * them, so work the caller enqueues afterwards sees the complete step. */
 int cb_step(cb_ctx* c, const float* inputs_dev, const int32_t* labels_dev);
 
 /* The synchronisation of Algorithm 1 for the pending gradients, in one
@@ -198,10 +202,13 @@ int cb_test_softmax_xent(int k, int b, int classes, const float* logits, const i
 
 /* --- instrumentation --------------------------------------------------- */
 
-/* While enabled, every kernel launch of the context is bracketed by a pair
- * of hipEvents on its stream, and the launch's algorithmic work (FLOPs of
- * the contraction, or bytes the operation must read and write) is recorded
- * with the kernel's name.  Costs a few microseconds per launch. */
+/* While enabled, every kernel launch of the context carries a start/stop
+ * hipEvent pair on its own dispatch (hipExtLaunchKernel), and the launch's
+ * algorithmic work (FLOPs of the contraction, or bytes the operation must
+ * read and write) is recorded with the kernel's name.  Instrumented steps
+ * run every kernel on the context's stream (the weight gradients do not
+ * overlap the data-gradient chain as they otherwise do), so each recorded
+ * duration is the kernel alone. */
 int cb_profile_enable(cb_ctx* c, int on);
 
 /* Waits for the stream and folds the records into per-kernel totals

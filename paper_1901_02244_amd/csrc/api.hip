@@ -439,8 +439,21 @@ struct cb_ctx {
   // weight-gradient split reductions of all layers, one launch per table
   std::vector<SplitTable> split_tables;
   std::vector<double> split_bytes;
+  // Weight gradients run on a second stream of the library's own (default
+  // priority), forked per layer once its output gradient is final and
+  // joined before the step ends, so they overlap the data-gradient chain.
+  hipStream_t side = nullptr;
+  std::vector<hipEvent_t> fork_ev;  // per operator (conv layers only)
+  hipEvent_t join_ev = nullptr;
 
   ~cb_ctx() {
+    if (side) {
+      (void)hipStreamSynchronize(side);
+      (void)hipStreamDestroy(side);
+    }
+    for (auto e : fork_ev)
+      if (e) (void)hipEventDestroy(e);
+    if (join_ev) (void)hipEventDestroy(join_ev);
     for (auto& r : recs) {
       (void)hipEventDestroy(r.a);
       (void)hipEventDestroy(r.b);
@@ -646,9 +659,19 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         const double flops = 2.0 * N * o.Ho * o.Wo * o.Co * o.Ci * o.R * o.R;
         const double wn = (double)o.Co * o.Ci * o.R * o.R;
         const double xin = (double)N * o.Ci * o.H * o.W, yout = (double)N * o.Co * o.Ho * o.Wo;
+        // dY of this layer is final here: its weight (and bias) gradient
+        // goes to the side stream; it reads dY and the layer's input and
+        // writes only this layer's slice of G and its own split partials
+        // (with instrumentation on, everything stays on the caller's stream,
+        // so each measured duration is the kernel alone)
+        hipStream_t ss = c->prof ? s : c->side;
+        if (!c->prof) {
+          CB_HIP(c, hipEventRecord(c->fork_ev[i], s));
+          CB_HIP(c, hipStreamWaitEvent(c->side, c->fork_ev[i], 0));
+        }
         if (o.bias)
           CB_LAUNCH(c, "channel_sum_k", 0.0, 4.0 * yout,
-                    channel_sum(grd(o.out), k, b, o.Co, o.Ho * o.Wo, G + o.b_off, p.Pp, s));
+                    channel_sum(grd(o.out), k, b, o.Co, o.Ho * o.Wo, G + o.b_off, p.Pp, ss));
         ConvBwdWeightArgs w;
         w.g = g;
         w.x = act(o.in);
@@ -661,7 +684,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
         {
           ProfScope ps(c);
           const char* nm = "conv_bwd_weight_k";
-          CB_HIP(c, conv_bwd_weight(w, s, &nm));
+          CB_HIP(c, conv_bwd_weight(w, ss, &nm));
           ps.done(nm, flops, 4.0 * (xin + yout + k * wn));
         }
         if (o.need_dx) {
@@ -690,15 +713,29 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
           ProfScope ps(c);
           const char* nm = "conv_bwd_data_k";
           CB_HIP(c, conv_bwd_data(d, s, &nm));
-          ps.done(nm, flops, 4.0 * (yout + k * wn + xin * (1.0 + o.dx_accumulate + o.dx_mask)));
+          // every tensor the kernel and its fused epilogue must move once: dY,
+          // the filters, dX (read too when accumulating), the ReLU mask, the
+          // residual gradient and the next batch norm's x (and y for its ReLU)
+          double moved = yout + k * wn + xin * (1.0 + o.dx_accumulate + o.dx_mask);
+          if (o.add_mode == ADD_SAME) moved += xin;
+          if (o.add_mode == ADD_SUBSAMPLE)
+            moved += (double)N * o.add_C * (o.H / o.add_st) * (o.W / o.add_st);
+          if (d.bn_part) moved += xin * (d.bn_y ? 2.0 : 1.0);
+          ps.done(nm, flops, 4.0 * moved);
         }
         break;
       }
     }
   }
+  hipStream_t ss = c->prof ? s : c->side;
   for (size_t i = 0; i < c->split_tables.size(); ++i)
     CB_LAUNCH(c, "reduce_splits_k", 0.0, c->split_bytes[i],
-              reduce_splits(c->split_tables[i], k, s));
+              reduce_splits(c->split_tables[i], k, ss));
+  // join: G is complete, and nothing reads this step's buffers any more
+  if (!c->prof) {
+    CB_HIP(c, hipEventRecord(c->join_ev, c->side));
+    CB_HIP(c, hipStreamWaitEvent(s, c->join_ev, 0));
+  }
   return CB_OK;
 }
 
@@ -827,6 +864,12 @@ int cb_create(const cb_model* m, int k, int b, float alpha, float lr, float mome
     }
   };
   dev(hipGetDevice(&c->device), "hipGetDevice");
+  dev(hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking), "hipStreamCreate");
+  c->fork_ev.assign(c->p.ops.size(), nullptr);
+  for (size_t i = 0; i < c->p.ops.size(); ++i)
+    if (c->p.ops[i].kind == OP_CONV)
+      dev(hipEventCreateWithFlags(&c->fork_ev[i], hipEventDisableTiming), "hipEventCreate");
+  dev(hipEventCreateWithFlags(&c->join_ev, hipEventDisableTiming), "hipEventCreate");
   const Plan& p = c->p;
   const size_t pbytes = (size_t)p.P * 4;
   // w0 is host memory the caller may free after this call, so the copies

@@ -14,13 +14,20 @@
 // same operation on dY with the filter transposed in its channels and
 // rotated by 180 degrees, which the weight loader applies (FLIP).
 //
-// Grid: x = row tiles of one replica (b * H / TH), y = output-channel tiles,
-// z = replica.  Epilogues match the implicit GEMM's: bias, ReLU and the
-// batch-norm partial sums of the forward; accumulate, residual add, ReLU
-// mask and the batch-norm backward partial sums of the data gradient.
+// Grid: as many workgroups as fit on the chip at once; each takes every G-th
+// tile (replica, output-channel tile, TH rows of one image) and prefetches
+// the next tile's inputs while it computes.  Epilogues match the implicit
+// GEMM's: bias, ReLU and the batch-norm partial sums of the forward;
+// accumulate, residual add, ReLU mask and the batch-norm backward partial
+// sums of the data gradient.
 #include "kernels.hpp"
 
+#include <algorithm>
 #include <string>
+
+#ifndef TAP_UNROLL
+#define TAP_UNROLL 9
+#endif
 
 namespace cbk {
 namespace {
@@ -66,38 +73,59 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   constexpr int M = TH * WW;              // output pixels per tile
   constexpr int TM = M / 64;              // 16-pixel blocks per wave (waves split M)
   constexpr int TN = BN / 16;
-  // Filter tile in LDS: [tap][ci][BN].  With BN = 32, odd input channels
-  // keep their two 16-column halves swapped, so the four lane groups of a
-  // read (four consecutive ci) do not pair up on the same banks.
-  constexpr int SWZ = BN == 32 ? 16 : 0;
+  // Filter tile in LDS, in the filter's own memory order so that stores
+  // are contiguous: forward [co][ci][tap] with row stride WS (146 = 144 + 2
+  // spreads the 16 columns x 4 channels of an operand read over the banks);
+  // data gradient [ci][co][8 - tap] (the flipped filter as stored) with row
+  // stride WS.
+  constexpr int WS = FLIP ? (BN == 16 ? 144 : 304) : CC * 9 + 2;
+  constexpr int WROWS = FLIP ? CC : BN;
+  constexpr int WRUN = FLIP ? BN * 9 : CC * 9;  // contiguous run of one row
   constexpr int NX = CC * HR * WP;        // input-tile elements per chunk
   constexpr int NXT = (NX + 255) / 256;
   constexpr int NW = 9 * CC * BN;         // filter elements per chunk
   constexpr int NWT = (NW + 255) / 256;
   static_assert(TM >= 1 && M % 64 == 0, "tile must cover whole 64-pixel wave strips");
   __shared__ __attribute__((aligned(16))) float xs[2][CC * CS];
-  __shared__ __attribute__((aligned(16))) float ws[2][9 * CC * BN];
+  __shared__ __attribute__((aligned(16))) float ws[2][WROWS * WS];
+  __shared__ double red[4][BN][2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4;
-  const int j = blockIdx.z, H = a.H, HW = H * WW;
+  const int H = a.H, HW = H * WW;
   const int tiles_img = H / TH;
-  const int img = blockIdx.x / tiles_img, oh0 = (blockIdx.x - img * tiles_img) * TH;
-  const int co0 = blockIdx.y * BN;
-  const int n_img = j * a.b + img;
-  const float* IN = a.in + (int64_t)n_img * a.Cin * HW;
-  const float* Wt = a.w + (int64_t)j * a.pstride;
+  const int rows_rep = a.b * tiles_img;            // row tiles of one replica
+  const int per_rep = rows_rep * (a.Cout / BN);    // tiles of one replica
+  const int T = a.k * per_rep;
   const int nchunk = a.Cin / CC;
 
+  // Tile t: replica, output-channel tile, then row tile (image-major), so
+  // the workgroups running together share filters and neighbouring rows.
+  struct Tile {
+    int j, co0, rt, img, oh0;
+  };
+  auto decode = [&](int t) {
+    Tile d;
+    d.j = t / per_rep;
+    const int r = t - d.j * per_rep;
+    const int ct = r / rows_rep;
+    d.rt = r - ct * rows_rep;
+    d.co0 = ct * BN;
+    d.img = d.rt / tiles_img;
+    d.oh0 = (d.rt - d.img * tiles_img) * TH;
+    return d;
+  };
+
   float rx[NXT], rw[NWT];
-  int rs[NWT];
-  auto load = [&](int c0) {
+  auto load = [&](const Tile& d, int c0) {
+    const float* IN = a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HW;
+    const float* Wt = a.w + (int64_t)d.j * a.pstride;
 #pragma unroll
     for (int u = 0; u < NXT; ++u) {
       const int e = tid + u * 256;
       float v = 0.f;
       if (e < NX) {
         const int ci = e / (HR * WP), rem = e - ci * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
-        const int ih = oh0 - 1 + hr, iw = wc - 1;
+        const int ih = d.oh0 - 1 + hr, iw = wc - 1;
         if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)WW)
           v = IN[(int64_t)(c0 + ci) * HW + ih * WW + iw];
       }
@@ -105,24 +133,18 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
     }
 #pragma unroll
     for (int u = 0; u < NWT; ++u) {
-      // e runs in memory order of the filter (tap fastest), so a wave's
-      // loads are contiguous; the slot keeps the [tap][ci][co] LDS order
+      // e runs in memory order of the filter slice: row (co, or ci when
+      // flipped), then a contiguous run within the row
       const int e = tid + u * 256;
       float v = 0.f;
-      int slot = 0;
       if (e < NW) {
-        if (!FLIP) {  // filter [out = co0+co][in = c0+ci][tap]
-          const int co = e / (CC * 9), rem = e - co * (CC * 9), ci = rem / 9, tap = rem - ci * 9;
-          v = Wt[((int64_t)(co0 + co) * a.Cin + c0 + ci) * 9 + tap];
-          slot = (tap * CC + ci) * BN + (co ^ ((ci & 1) ? SWZ : 0));
-        } else {      // original filter [its out = c0+ci][its in = co0+co][8 - tap]
-          const int ci = e / (BN * 9), rem = e - ci * (BN * 9), co = rem / 9, t = rem - co * 9;
-          v = Wt[((int64_t)(c0 + ci) * a.Cout + co0 + co) * 9 + t];
-          slot = ((8 - t) * CC + ci) * BN + (co ^ ((ci & 1) ? SWZ : 0));
-        }
+        const int row = e / WRUN, rem = e - row * WRUN;
+        if (!FLIP)  // filter [out = co0+row][in = c0 .. c0+CC)[tap]
+          v = Wt[((int64_t)(d.co0 + row) * a.Cin + c0) * 9 + rem];
+        else        // filter [its out = c0+row][its in = co0 .. co0+BN)[tap]
+          v = Wt[((int64_t)(c0 + row) * a.Cout + d.co0) * 9 + rem];
       }
       rw[u] = v;
-      rs[u] = slot;
     }
   };
   auto store = [&](int buf) {
@@ -135,8 +157,13 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       }
     }
 #pragma unroll
-    for (int u = 0; u < NWT; ++u)
-      if (tid + u * 256 < NW) ws[buf][rs[u]] = rw[u];
+    for (int u = 0; u < NWT; ++u) {
+      const int e = tid + u * 256;
+      if (e < NW) {
+        const int row = e / WRUN;
+        ws[buf][row * WS + (e - row * WRUN)] = rw[u];
+      }
+    }
   };
 
   // lane bases: pixel of each of this wave's 16-pixel blocks, and column
@@ -147,135 +174,173 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
     const int ohl = m / WW, ow = m - ohl * WW;
     xbase[t] = kq * CS + ohl * WP + ow;
   }
-  const int wbase = kq * BN + (lane & 15);
-  const int wswz = (kq & 1) ? SWZ : 0;
+  // B operand of lane (kq, l16): input channel cg*4 + kq, output channel
+  // u*16 + l16 of the tile
+  const int wbase = FLIP ? kq * WS + (lane & 15) * 9 : (lane & 15) * WS + kq * 9;
+
+  // Epilogue operands of the data gradient (ReLU mask, the next batch
+  // norm's x and y), loaded before the tile's last MFMAs so their latency
+  // overlaps the contraction: four consecutive pixels of one channel per
+  // lane and block.
+  v4f e_mask[TM][TN], e_x[TM][TN], e_y[TM][TN];
+  auto gofs = [&](const Tile& d, int t, int u) {  // (plane offset, first pixel)
+    const int co = d.co0 + u * 16 + (lane & 15);
+    const int p0 = d.oh0 * WW + (wave * TM + t) * 16 + 4 * kq;
+    return (int64_t)((d.j * a.b + d.img) * a.Cout + co) * HW + p0;
+  };
+  auto prefetch_epilogue = [&](const Tile& d) {
+    if (!FLIP) return;
+#pragma unroll
+    for (int t = 0; t < TM; ++t)
+#pragma unroll
+      for (int u = 0; u < TN; ++u) {
+        const int64_t g = gofs(d, t, u);
+        if (a.mask) e_mask[t][u] = *reinterpret_cast<const v4f*>(a.mask + g);
+        if (a.bn_part) {
+          e_x[t][u] = *reinterpret_cast<const v4f*>(a.bn_x + g);
+          if (a.bn_y) e_y[t][u] = *reinterpret_cast<const v4f*>(a.bn_y + g);
+        }
+      }
+  };
 
   v4f acc[TM][TN];
+  auto epilogue = [&](const Tile& d) {
+    // acc[t][u][i] is pixel (wave*TM + t)*16 + 4*kq + i, channel
+    // co0 + u*16 + (lane & 15) of the tile
+    double s1[TN], s2[TN];
 #pragma unroll
-  for (int x = 0; x < TM; ++x)
+    for (int u = 0; u < TN; ++u) s1[u] = s2[u] = 0.0;
 #pragma unroll
-    for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < TN; ++u) {
+      const int co = d.co0 + u * 16 + (lane & 15);
+      float bv = 0.f, bm = 0.f, bi = 0.f;
+      if (!FLIP && a.bias) bv = a.bias[(int64_t)d.j * a.pstride + co];
+      if (FLIP && a.bn_part) {
+        bm = a.bn_mean[d.j * a.Cout + co];
+        bi = a.bn_istd[d.j * a.Cout + co];
+      }
+#pragma unroll
+      for (int t = 0; t < TM; ++t) {
+        const int64_t g = gofs(d, t, u);
+        v4f v = acc[t][u];
+        if (!FLIP) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float e = v[i] + bv;
+            if (a.relu) e = e > 0.f ? e : 0.f;
+            v[i] = e;
+            s1[u] += (double)e;
+            s2[u] += (double)e * e;
+          }
+          *reinterpret_cast<v4f*>(a.out + g) = v;
+        } else {
+          if (a.accumulate) v += *reinterpret_cast<const v4f*>(a.out + g);
+          if (a.add_mode == ADD_SAME) {
+            v += *reinterpret_cast<const v4f*>(a.add + g);
+          } else if (a.add_mode == ADD_SUBSAMPLE) {
+            const int st = a.add_st;
+            const int p0 = d.oh0 * WW + (wave * TM + t) * 16 + 4 * kq;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int p = p0 + i, ih = p / WW, iw = p - ih * WW;
+              if (ih % st == 0 && iw % st == 0)
+                v[i] += a.add[(((int64_t)(d.j * a.b + d.img) * a.add_C + co) * (H / st) + ih / st) *
+                                  (WW / st) + iw / st];
+            }
+          }
+          if (a.mask)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (!(e_mask[t][u][i] > 0.f)) v[i] = 0.f;
+          *reinterpret_cast<v4f*>(a.out + g) = v;
+          if (a.bn_part) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float dd = (!a.bn_y || e_y[t][u][i] > 0.f) ? v[i] : 0.f;
+              const float xh = (e_x[t][u][i] - bm) * bi;
+              s1[u] += (double)dd;
+              s2[u] += (double)dd * xh;
+            }
+          }
+        }
+      }
+    }
+    double* part = FLIP ? a.bn_part : a.stats;
+    if (!part) return;
+    // per-channel partial sums of the tile: lanes of a column by xor
+    // butterfly, then the four waves in order.  (Every chunk ends with a
+    // barrier, so the previous tile's reads of red are done.)
+#pragma unroll
+    for (int u = 0; u < TN; ++u) {
+      double x = s1[u], y = s2[u];
+      x += shfl_xor_d(x, 16);
+      y += shfl_xor_d(y, 16);
+      x += shfl_xor_d(x, 32);
+      y += shfl_xor_d(y, 32);
+      if (lane < 16) {
+        red[wave][u * 16 + lane][0] = x;
+        red[wave][u * 16 + lane][1] = y;
+      }
+    }
+    __syncthreads();
+    if (tid < BN) {
+      const double x = ((red[0][tid][0] + red[1][tid][0]) + red[2][tid][0]) + red[3][tid][0];
+      const double y = ((red[0][tid][1] + red[1][tid][1]) + red[2][tid][1]) + red[3][tid][1];
+      double* o = part + (((int64_t)d.j * a.Cout + d.co0 + tid) * rows_rep + d.rt) * 2;
+      o[0] = x;
+      o[1] = y;
+    }
+  };
 
-  load(0);
+  // Workgroup w takes tiles w, w + G, w + 2G, ...  Every (tile, chunk) item
+  // prefetches the next item's inputs into registers before its MFMAs.
+  const int G = gridDim.x;
+  int t = blockIdx.x;
+  Tile d = decode(t);
+  load(d, 0);
   store(0);
   __syncthreads();
-  for (int c = 0; c < nchunk; ++c) {
-    const int cur = c & 1;
-    if (c + 1 < nchunk) load((c + 1) * CC);
-    const float* X = xs[cur];
-    const float* Wl = ws[cur];
+  int cur = 0;
+  while (true) {
 #pragma unroll
-    for (int tap = 0; tap < 9; ++tap) {
-      const int r = tap / 3, s = tap - r * 3;
+    for (int x = 0; x < TM; ++x)
 #pragma unroll
-      for (int cg = 0; cg < CC / 4; ++cg) {
-        float av[TM], bv[TN];
+      for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+    const bool more = t + G < T;
+    const Tile dn = more ? decode(t + G) : d;
+    for (int c = 0; c < nchunk; ++c) {
+      const bool last = c + 1 == nchunk;
+      const bool has_next = !last || more;
+      if (has_next) load(last ? dn : d, last ? 0 : (c + 1) * CC);
+      if (last) prefetch_epilogue(d);
+      const float* X = xs[cur];
+      const float* Wl = ws[cur];
+#pragma unroll TAP_UNROLL
+      for (int tap = 0; tap < 9; ++tap) {
+        const int r = tap / 3, s = tap - r * 3;
 #pragma unroll
-        for (int t = 0; t < TM; ++t) av[t] = X[xbase[t] + cg * 4 * CS + r * WP + s];
+        for (int cg = 0; cg < CC / 4; ++cg) {
+          float av[TM], bv[TN];
 #pragma unroll
-        for (int u = 0; u < TN; ++u) bv[u] = Wl[wbase + (tap * CC + cg * 4) * BN + ((u * 16) ^ wswz)];
+          for (int x = 0; x < TM; ++x) av[x] = X[xbase[x] + cg * 4 * CS + r * WP + s];
 #pragma unroll
-        for (int t = 0; t < TM; ++t)
+          for (int u = 0; u < TN; ++u)
+            bv[u] = FLIP ? Wl[wbase + cg * 4 * WS + u * 144 + (8 - tap)]
+                         : Wl[wbase + u * 16 * WS + cg * 36 + tap];
 #pragma unroll
-          for (int u = 0; u < TN; ++u) acc[t][u] = mfma4(av[t], bv[u], acc[t][u]);
-      }
-    }
-    if (c + 1 < nchunk) store(cur ^ 1);
-    __syncthreads();
-  }
-
-  // epilogue: acc[t][u][i] is pixel (wave*TM + t)*16 + 4*kq + i, channel
-  // co0 + u*16 + (lane & 15) of this tile -- four consecutive pixels of one
-  // channel per lane, so every operand moves as one 16-byte access
-  float* OUT = a.out + (int64_t)n_img * a.Cout * HW;
-  double s1[TN], s2[TN];
+          for (int x = 0; x < TM; ++x)
 #pragma unroll
-  for (int u = 0; u < TN; ++u) s1[u] = s2[u] = 0.0;
-#pragma unroll
-  for (int u = 0; u < TN; ++u) {
-    const int co = co0 + u * 16 + (lane & 15);
-    float bv = 0.f, bm = 0.f, bi = 0.f;
-    if (!FLIP && a.bias) bv = a.bias[(int64_t)j * a.pstride + co];
-    if (FLIP && a.bn_part) {
-      bm = a.bn_mean[j * a.Cout + co];
-      bi = a.bn_istd[j * a.Cout + co];
-    }
-#pragma unroll
-    for (int t = 0; t < TM; ++t) {
-      const int p0 = oh0 * WW + (wave * TM + t) * 16 + 4 * kq;  // first pixel in the plane
-      const int64_t idx = (int64_t)co * HW + p0;
-      v4f v = acc[t][u];
-      if (!FLIP) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float e = v[i] + bv;
-          if (a.relu) e = e > 0.f ? e : 0.f;
-          v[i] = e;
-          s1[u] += (double)e;
-          s2[u] += (double)e * e;
-        }
-        *reinterpret_cast<v4f*>(OUT + idx) = v;
-      } else {
-        const int64_t gidx = (int64_t)n_img * a.Cout * HW + idx;
-        if (a.accumulate) v += *reinterpret_cast<const v4f*>(OUT + idx);
-        if (a.add_mode == ADD_SAME) {
-          v += *reinterpret_cast<const v4f*>(a.add + gidx);
-        } else if (a.add_mode == ADD_SUBSAMPLE) {
-          const int st = a.add_st;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int p = p0 + i, ih = p / WW, iw = p - ih * WW;
-            if (ih % st == 0 && iw % st == 0)
-              v[i] += a.add[(((int64_t)n_img * a.add_C + co) * (H / st) + ih / st) * (WW / st) +
-                            iw / st];
-          }
-        }
-        if (a.mask) {
-          const v4f m = *reinterpret_cast<const v4f*>(a.mask + gidx);
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (!(m[i] > 0.f)) v[i] = 0.f;
-        }
-        *reinterpret_cast<v4f*>(OUT + idx) = v;
-        if (a.bn_part) {
-          const v4f xv = *reinterpret_cast<const v4f*>(a.bn_x + gidx);
-          v4f yv = v4f{1.f, 1.f, 1.f, 1.f};
-          if (a.bn_y) yv = *reinterpret_cast<const v4f*>(a.bn_y + gidx);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float d = (yv[i] > 0.f) ? v[i] : 0.f;
-            const float xh = (xv[i] - bm) * bi;
-            s1[u] += (double)d;
-            s2[u] += (double)d * xh;
-          }
+            for (int u = 0; u < TN; ++u) acc[x][u] = mfma4(av[x], bv[u], acc[x][u]);
         }
       }
+      if (has_next) store(cur ^ 1);
+      __syncthreads();
+      cur ^= 1;
     }
-  }
-  double* part = FLIP ? a.bn_part : a.stats;
-  if (!part) return;
-  // per-channel partial sums of the tile: lanes of a column by xor
-  // butterfly, then the four waves in order
-  __shared__ double red[4][BN][2];
-#pragma unroll
-  for (int u = 0; u < TN; ++u) {
-    double x = s1[u], y = s2[u];
-    x += shfl_xor_d(x, 16);
-    y += shfl_xor_d(y, 16);
-    x += shfl_xor_d(x, 32);
-    y += shfl_xor_d(y, 32);
-    if (lane < 16) {
-      red[wave][u * 16 + lane][0] = x;
-      red[wave][u * 16 + lane][1] = y;
-    }
-  }
-  __syncthreads();
-  if (tid < BN) {
-    const double x = ((red[0][tid][0] + red[1][tid][0]) + red[2][tid][0]) + red[3][tid][0];
-    const double y = ((red[0][tid][1] + red[1][tid][1]) + red[2][tid][1]) + red[3][tid][1];
-    double* o = part + (((int64_t)j * a.Cout + co0 + tid) * gridDim.x + blockIdx.x) * 2;
-    o[0] = x;
-    o[1] = y;
+    epilogue(d);
+    if (!more) break;
+    t += G;
+    d = dn;
   }
 }
 
@@ -437,8 +502,22 @@ const char* direct_name() {
 
 template <int WW, int TH, int BN, int CC, bool FLIP>
 hipError_t launch(const DirectArgs& a, hipStream_t s, const char** name) {
-  dim3 grid((unsigned)(a.b * (a.H / TH)), (unsigned)(a.Cout / BN), (unsigned)a.k);
-  klaunch((conv3x3_k<WW, TH, BN, CC, FLIP>), grid, dim3(256), 0, s, a);
+  // as many workgroups as are resident at once, each taking an equal share
+  // of the tiles (the last share may be one short)
+  static int resident = 0;
+  if (!resident) {
+    int per_cu = 0, cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv3x3_k<WW, TH, BN, CC, FLIP>, 256,
+                                                     0) != hipSuccess)
+      return hipErrorInvalidValue;
+    resident = std::max(1, per_cu) * std::max(1, cus);
+  }
+  const int64_t T = (int64_t)a.k * a.b * (a.H / TH) * (a.Cout / BN);
+  const int64_t per = (T + resident - 1) / resident;
+  const int64_t G = (T + per - 1) / per;
+  klaunch(conv3x3_k<WW, TH, BN, CC, FLIP>, dim3((unsigned)G), dim3(256), 0, s, a);
   if (name) *name = direct_name<WW, TH, BN, CC, FLIP>();
   return hipGetLastError();
 }

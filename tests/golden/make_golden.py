@@ -5,7 +5,8 @@ synthetic inputs of ``workloads``; nothing is read from the GPU library.
 Run from the repository root:
 
     python tests/golden/make_golden.py lenet_envelope
-    python tests/golden/make_golden.py resnet32_z100     # ~1 h single-threaded
+    python tests/golden/make_golden.py resnet32_z100     # ~35 min single-threaded
+    python tests/golden/make_golden.py resnet32_z10      # ~4 min
     python tests/golden/make_golden.py resnet32_envelope # ~1 h
     python tests/golden/make_golden.py resnet50_sampled  # ~10 min
 
@@ -15,8 +16,8 @@ Jobs:
     relative L2 distance of the two central models at several steps.  Any
     fp32 implementation that sums in another order can differ from the
     oracle by about this much; the long-run parity bound uses it.
-  resnet32_z100: the central model after 100 SMA iterations of ResNet-32,
-    k = 4 learners of batch 32 (float32 .npy).
+  resnet32_z100 / resnet32_z10: the central model after 100 (10) SMA
+    iterations of ResNet-32, k = 4 learners of batch 32 (float32 .npy).
   resnet50_sampled: learner 0's loss and sampled gradient entries after one
     forward/backward pass of ResNet-50 on 224x224 images, b = 32.
 """
@@ -77,15 +78,16 @@ def envelope(wk, out_name, steps=100):
     print(doc)
 
 
-def resnet32_z100():
+def resnet32_z(steps):
     wk = wl.RESNET32_K4
     t0 = time.time()
-    s, kept = run_sma(wk, 100, w0_of(wk), keep=(1, 100))
-    np.save(os.path.join(HERE, "resnet32_k4_b32_z100.npy"), kept[100].astype(np.float32))
-    json.dump({"workload": wk.name, "steps": 100, "seconds": round(time.time() - t0),
-               "file": "resnet32_k4_b32_z100.npy", "dtype": "float32 (oracle fp64 rounded)",
+    s, kept = run_sma(wk, steps, w0_of(wk), keep=(steps,))
+    name = f"resnet32_k4_b32_z{steps}"
+    np.save(os.path.join(HERE, name + ".npy"), kept[steps].astype(np.float32))
+    json.dump({"workload": wk.name, "steps": steps, "seconds": round(time.time() - t0),
+               "file": name + ".npy", "dtype": "float32 (oracle fp64 rounded)",
                "loss_last": [float(v) for v in s.loss()]},
-              open(os.path.join(HERE, "resnet32_k4_b32_z100.json"), "w"), indent=1)
+              open(os.path.join(HERE, name + ".json"), "w"), indent=1)
 
 
 def resnet50_sampled(per_tensor=24):
@@ -118,7 +120,9 @@ if __name__ == "__main__":
     elif job == "resnet32_envelope":
         envelope(wl.RESNET32_K4, "resnet32_k4_b32_envelope.json")
     elif job == "resnet32_z100":
-        resnet32_z100()
+        resnet32_z(100)
+    elif job == "resnet32_z10":
+        resnet32_z(10)
     elif job == "resnet50_sampled":
         resnet50_sampled()
     else:
