@@ -28,6 +28,9 @@
 #ifndef TAP_UNROLL
 #define TAP_UNROLL 9
 #endif
+#ifndef CG_UNROLL
+#define CG_UNROLL 4
+#endif
 
 namespace cbk {
 namespace {
@@ -318,7 +321,7 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
 #pragma unroll TAP_UNROLL
       for (int tap = 0; tap < 9; ++tap) {
         const int r = tap / 3, s = tap - r * 3;
-#pragma unroll
+#pragma unroll CG_UNROLL
         for (int cg = 0; cg < CC / 4; ++cg) {
           float av[TM], bv[TN];
 #pragma unroll

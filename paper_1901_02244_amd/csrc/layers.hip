@@ -413,37 +413,35 @@ __global__ __launch_bounds__(256) void gap_bwd_k(const float* dy, int64_t n, int
 
 // One block per learner: mean over its b images of -log softmax(o)_y and
 // the gradient (softmax(o) - onehot(y)) / b (Eq. 2).
+// One block per learner; wave w takes rows w, w+4, ...  Each row's max
+// and sum of exponentials are wave reductions (no block barriers); the
+// waves' fp64 loss partials, each summed in row order, are combined in wave
+// order.
 __global__ __launch_bounds__(256) void softmax_xent_k(const float* logits, const int32_t* labels,
                                                       int b, int classes, float* dlogits,
                                                       float* loss) {
-  __shared__ float red[4];
-  const int j = blockIdx.x, t = threadIdx.x, w = t >> 6;
+  __shared__ double red[4];
+  const int j = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   double tot = 0.0;
-  for (int i = 0; i < b; ++i) {
+  for (int i = w; i < b; i += 4) {
     const int64_t row = (int64_t)(j * b + i) * classes;
     const float* o = logits + row;
     float mx = -INFINITY;
-    for (int c = t; c < classes; c += 256) mx = fmaxf(mx, o[c]);
+    for (int c = lane; c < classes; c += 64) mx = fmaxf(mx, o[c]);
     mx = wave_max_f(mx);
-    __syncthreads();
-    if ((t & 63) == 0) red[w] = mx;
-    __syncthreads();
-    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
     float se = 0.f;
-    for (int c = t; c < classes; c += 256) se += expf(o[c] - mx);
+    for (int c = lane; c < classes; c += 64) se += expf(o[c] - mx);
     se = wave_sum_f(se);
-    __syncthreads();
-    if ((t & 63) == 0) red[w] = se;
-    __syncthreads();
-    se = (red[0] + red[1]) + (red[2] + red[3]);
     const float lse = mx + logf(se);
     const int y = labels[j * b + i];
     const bool yok = (unsigned)y < (unsigned)classes;
-    for (int c = t; c < classes; c += 256)
+    for (int c = lane; c < classes; c += 64)
       dlogits[row + c] = (expf(o[c] - lse) - (c == y ? 1.f : 0.f)) / b;
-    if (t == 0) tot += yok ? (double)(lse - o[y]) : (double)NAN;
+    if (lane == 0) tot += yok ? (double)(lse - o[y]) : (double)NAN;
   }
-  if (t == 0) loss[j] = (float)(tot / b);
+  if (lane == 0) red[w] = tot;
+  __syncthreads();
+  if (threadIdx.x == 0) loss[j] = (float)((((red[0] + red[1]) + red[2]) + red[3]) / b);
 }
 
 }  // namespace
