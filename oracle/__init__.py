@@ -68,6 +68,11 @@ def lib():
         L.cbref_sync.argtypes = [_P]
         L.cbref_sma_apply.argtypes = [_P, _P]
         L.cbref_set_state.argtypes = [_P, _P, _P, _P, _P]
+        L.cbref_set_lr.argtypes = [_P, ctypes.c_double]
+        L.cbref_restart.argtypes = [_P]
+        L.cbref_set_learners.argtypes = [_P, ctypes.c_int, ctypes.c_double]
+        L.cbref_tuner_next.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_double,
+                                       ctypes.c_double, ctypes.c_int]
         for name in ("cbref_get_central", "cbref_get_prev_central", "cbref_get_loss"):
             getattr(L, name).argtypes = [_P, _P]
         for name in ("cbref_get_replica", "cbref_get_grad"):
@@ -193,6 +198,18 @@ class SMA:
         Z, Zp = _f64(Z), _f64(Zp)
         lib().cbref_set_state(self._c, _ptr(W), _ptr(Wp), _ptr(Z), _ptr(Zp))
 
+    def set_lr(self, lr):
+        lib().cbref_set_lr(self._c, float(lr))
+
+    def restart(self):
+        lib().cbref_restart(self._c)
+
+    def set_learners(self, k, alpha):
+        rc = lib().cbref_set_learners(self._c, int(k), float(alpha))
+        if rc == 0:
+            self.k = int(k)
+        return rc
+
     def central(self):
         o = np.empty(self.P)
         lib().cbref_get_central(self._c, _ptr(o))
@@ -217,6 +234,11 @@ class SMA:
         o = np.empty(self.k)
         lib().cbref_get_loss(self._c, _ptr(o))
         return o
+
+
+def tuner_next(l, t, t_prev, threshold, l_max):
+    """Algorithm 2, one observation (see cbref_tuner_next)."""
+    return lib().cbref_tuner_next(int(l), float(t), float(t_prev), float(threshold), int(l_max))
 
 
 # --- layer primitives, for pinning each against a library routine -------

@@ -1046,6 +1046,64 @@ int cbref_sync(cbref_ctx* c) {
   return 0;
 }
 
+/* A new learning rate gamma for the following updates (the step-wise
+ * schedule of Sec. 3.2: gamma may change between iterations). */
+int cbref_set_lr(cbref_ctx* c, double lr) {
+  c->lr = lr;
+  return 0;
+}
+
+/* Restart of SMA (Sec. 3.2): Algorithm 1 starts again with the latest
+ * central model as its initial model, so every replica, its previous
+ * value and z_prev become z (zero velocity).  A gradient still pending
+ * from an unsynchronised step is dropped. */
+int cbref_restart(cbref_ctx* c) {
+  for (int64_t e = 0; e < c->P; ++e) {
+    const double z = c->Z[e];
+    c->Zp[e] = z;
+    for (int j = 0; j < c->k; ++j) c->W[(size_t)j * c->P + e] = c->Wprev[(size_t)j * c->P + e] = z;
+  }
+  c->pending = 0;
+  return 0;
+}
+
+/* Changes the number of learners between iterations (Sec. 3.4 / 4.4): a
+ * new learner's replica is initialised with the latest central model z
+ * (and so is its previous value); removing learners drops the most recently
+ * added ones.  alpha is the correction factor used from now on.  Returns
+ * -4 while a gradient is pending, -1 for k < 1. */
+int cbref_set_learners(cbref_ctx* c, int k, double alpha) {
+  if (k < 1) return -1;
+  if (c->pending) return -4;
+  const int64_t n = c->P;
+  double* W = dalloc((size_t)k * n);
+  double* Wprev = dalloc((size_t)k * n);
+  double* G = dalloc((size_t)k * n);
+  double* loss = dalloc(k);
+  for (int j = 0; j < k; ++j)
+    for (int64_t e = 0; e < n; ++e) {
+      const size_t i = (size_t)j * n + e;
+      W[i] = j < c->k ? c->W[i] : c->Z[e];
+      Wprev[i] = j < c->k ? c->Wprev[i] : c->Z[e];
+    }
+  free(c->W); free(c->Wprev); free(c->G); free(c->loss);
+  c->W = W; c->Wprev = Wprev; c->G = G; c->loss = loss;
+  c->k = k;
+  c->alpha = alpha;
+  return 0;
+}
+
+/* Algorithm 2 (Sec. 3.4), one observation: l learners gave throughput t;
+ * t_prev is the throughput observed before.  Returns l + 1 if the increase
+ * exceeds the threshold, l - 1 if throughput fell (never below one
+ * learner), l otherwise; the caller then keeps t as the next t_prev.
+ * l_max bounds the increase (the capacity the caller provisioned). */
+int cbref_tuner_next(int l, double t, double t_prev, double threshold, int l_max) {
+  if (t - t_prev > threshold) return l < l_max ? l + 1 : l;
+  if (t < t_prev && l > 1) return l - 1;
+  return l;
+}
+
 /* Test hook: take grads [k][P] as the learners' raw gradients, then sync. */
 int cbref_sma_apply(cbref_ctx* c, const double* grads) {
   memcpy(c->G, grads, sizeof(double) * (size_t)c->k * c->P);
