@@ -142,6 +142,117 @@ def time_training(wk, steps, warmup, ring=8, prof_steps=0):
     return ms, wall, loss
 
 
+def _context(wk, k=None, alpha=None, momentum=None, learner_momentum=0.0, capacity=None):
+    import paper_1901_02244_amd as cb
+    import workloads as wl
+
+    k = wk.k if k is None else k
+    m = cb.model(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes,
+                 learner_momentum=learner_momentum)
+    w0 = wl.init_w0(cb.cb_tensor_layout(m), wk.seed)
+    cap = capacity or k
+    ctx = cb.Context(m, cap, wk.b, 1.0 / cap if alpha is None else alpha, wk.lr,
+                     wk.momentum if momentum is None else momentum, w0)
+    if cap != k:
+        ctx.cb_set_learners(k, 1.0 / k if alpha is None else alpha)
+    return ctx
+
+
+def _timed(ctx, wk, iters, tau, ring=8):
+    """ms per iteration with a synchronisation every tau iterations
+    (tau = 0: never)."""
+    import torch
+    import workloads as wl
+
+    n_img = ctx.k * wk.b
+    xs, ys = [], []
+    for t in range(ring):
+        x, y = wl.batch(n_img, wk.in_c, wk.in_h, wk.in_w, wk.num_classes, wk.seed, t)
+        xs.append(torch.from_numpy(x).cuda())
+        ys.append(torch.from_numpy(y).cuda())
+    def run(n, t0):
+        for i in range(n):
+            ctx.cb_step(xs[(t0 + i) % ring], ys[(t0 + i) % ring])
+            if tau and (t0 + i + 1) % tau == 0:
+                ctx.cb_sync()
+    run(3 * max(1, tau), 0)  # warm-up; ends on a synchronisation when tau > 0
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    run(iters, 0)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / iters
+
+
+def sync_interval_sweep(wk, iters=96):
+    """Throughput with a synchronisation every tau iterations and with none
+    (the paper's sync-overhead experiment, on one GPU): the unsynchronised
+    steps are local steps of each learner."""
+    out = {}
+    for tau in (1, 2, 4, 8, 0):
+        ctx = _context(wk)
+        ms = _timed(ctx, wk, iters, tau)
+        ctx.close()
+        out["none" if tau == 0 else str(tau)] = {"ms_per_step": round(ms, 4),
+                                                 "images_per_s": round(wk.n_images / ms * 1e3, 1)}
+        log(f"[bench] sync every {tau or 'never'}: {ms:.3f} ms/step, {wk.n_images / ms * 1e3:.0f} images/s")
+    return out
+
+
+def autotune(wk, capacity=32, window=40, threshold=1000.0, max_obs=24):
+    """Algorithm 2 online on one GPU: start with one learner, observe the
+    throughput of each window of iterations, and change the number of
+    learners by the library's decision rule (new learners start from z).
+    The rule keeps probing around the best count, so the run reports the
+    range of learner counts of its last 8 observations."""
+    import paper_1901_02244_amd as cb
+
+    ctx = _context(wk, k=1, capacity=capacity)
+    t_prev, trail = 0.0, []
+    for _ in range(max_obs):
+        ms = _timed(ctx, wk, window, 1)
+        t = ctx.k * wk.b / ms * 1e3
+        trail.append([ctx.k, round(t, 1)])
+        nl = cb.cb_tuner_next(ctx.k, t, t_prev, threshold, capacity)
+        t_prev = t
+        if nl != ctx.k:
+            ctx.cb_set_learners(nl, 1.0 / nl)
+    ctx.close()
+    log(f"[bench] auto-tuner: {trail}")
+    last = [k for k, _ in trail[-8:]]
+    return {"threshold_images_per_s": threshold, "window_iterations": window,
+            "capacity": capacity, "trail_k_images_per_s": trail,
+            "k_range_last_8": [min(last), max(last)]}
+
+
+def ssgd_baseline(wk, iters=100):
+    """S-SGD on the same kernels: one replica with the aggregate batch k*b
+    and momentum SGD (Eq. 3: one learner, alpha = 0, learner momentum mu)."""
+    import dataclasses
+
+    one = dataclasses.replace(wk, k=1, b=wk.k * wk.b)
+    ctx = _context(one, k=1, alpha=0.0, learner_momentum=wk.momentum)
+    ms = _timed(ctx, one, iters, 1)
+    ctx.close()
+    log(f"[bench] S-SGD baseline (1 replica, batch {one.b}): {ms:.3f} ms/step, "
+        f"{one.b / ms * 1e3:.0f} images/s")
+    return {"batch": one.b, "ms_per_step": round(ms, 4), "images_per_s": round(one.b / ms * 1e3, 1)}
+
+
+def lenet_latency(iters=200):
+    """LeNet-5, k = 8 learners of 16: launch/latency-bound; us per iteration
+    and kernel launches per iteration."""
+    import workloads as wl
+
+    wk = wl.LENET_K8
+    ms, _, _, prof = time_training(wk, iters, 10, prof_steps=10)
+    launches = sum(v[0] for v in prof.values())
+    log(f"[bench] LeNet k=8 b=16: {ms * 1e3:.1f} us/iteration, {launches:.0f} launches/iteration")
+    return {"us_per_iteration": round(ms * 1e3, 2), "launches_per_iteration": launches,
+            "images_per_s": round(wk.n_images / ms * 1e3, 1)}
+
+
 def sma_micro(steps=20, warmup=3):
     """Fused SMA kernel alone on ResNet-50's P with k = 32 replicas."""
     import torch
@@ -298,6 +409,12 @@ def main():
             sms, swall, _ = time_training(w, args.sweep_steps, 3)
             sweep[str(k)] = {"ms_per_step": round(sms, 4), "images_per_s": round(w.n_images / (sms / 1e3), 1)}
             log(f"[bench] sweep b=16 k={k}: {sms:.3f} ms/step, {w.n_images / (sms / 1e3):.0f} images/s")
+    extra = {}
+    if not args.no_sweep:
+        extra["sync_interval_sweep"] = sync_interval_sweep(wk)
+        extra["ssgd_baseline_same_kernels"] = ssgd_baseline(wk)
+        extra["autotune_alg2_b16"] = autotune(wl.RESNET32_SWEEP)
+        extra["lenet_k8_b16"] = lenet_latency()
     micro = None
     if not args.no_micro:
         micro = sma_micro()
@@ -328,6 +445,7 @@ def main():
         "kernels_per_step": kernels,
         "k_sweep_b16": sweep,
         "k_sweep_best": max(sweep, key=lambda k: sweep[k]["images_per_s"]) if sweep else None,
+        **extra,
         "sma_microbench": micro,
         "cpu_baseline": cpu,
         "final_loss": [round(float(v), 4) for v in loss],

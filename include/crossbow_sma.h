@@ -81,12 +81,14 @@ int cb_tensor_info(const cb_model* m, int idx, int64_t* offset, int* kind, int* 
                    int* dims4);
 
 /* Bytes of device workspace that cb_create needs for k learners of batch b
- * (replicas, gradients, z, z_prev, activations, scratch); 0 on bad input. */
+ * (replicas, gradients, z, z_prev, activations, scratch) -- enough for any
+ * number of active learners up to k (cb_set_learners); 0 on bad input. */
 size_t cb_workspace_bytes(const cb_model* m, int k, int b);
 
 /* Algorithm 1, initialisation: z <- w0, and (readings where the algorithm
  * is silent) z_prev <- w0 and every replica w_j <- w0.
- *   k >= 1 learners, b >= 1 images each; alpha is the correction weight
+ *   k >= 1 learners (also the capacity for cb_set_learners), b >= 1 images
+ *   each; alpha is the correction weight
  *   (about 1/k, Sec. 3.2), lr the learning rate gamma, momentum the Polyak
  *   momentum mu on z; all must be finite.
  *   w0_host: P floats in the order above (copied; the caller keeps it).
@@ -146,6 +148,42 @@ int cb_sma_apply(cb_ctx* c, const float* grads_dev);
  * w_prev (learner momentum only) is set equal to W.  Clears any pending
  * gradient.  Blocks until the copies are done. */
 int cb_set_state(cb_ctx* c, const float* W_host, const float* z_host, const float* zprev_host);
+
+/* --- control between iterations ----------------------------------------
+ * These change the training process between iterations of Algorithm 1 and
+ * are enqueued on the context's stream like the rest. */
+
+/* The learning rate gamma for the following updates: the step-wise
+ * schedule of Sec. 3.2 changes gamma between iterations.  lr must be
+ * finite. */
+int cb_set_lr(cb_ctx* c, float lr);
+
+/* Restart of SMA (Sec. 3.2): Algorithm 1 starts again from the latest
+ * central model z as its initial model -- every active replica (and its
+ * previous value) and z_prev become z.  A gradient pending from an
+ * unsynchronised cb_step is dropped. */
+int cb_restart(cb_ctx* c);
+
+/* Changes the number of active learners to k, 1 <= k <= the k given to
+ * cb_create, between iterations (Sec. 3.4; the tuner of Sec. 4.4 adds a
+ * learner at an iteration barrier).  A new learner's replica and its
+ * previous value are the latest central model z; removing learners drops
+ * the most recently added ones (the paper does not say which).  alpha is
+ * the correction weight from now on (about 1/k).  cb_step then takes
+ * k*b images.  CB_ESTATE while a gradient is pending (call cb_sync first),
+ * CB_EINVAL for k out of range.  Allocates nothing: the workspace was
+ * sized for every k up to the capacity. */
+int cb_set_learners(cb_ctx* c, int k, float alpha);
+
+/* The number of active learners. */
+int cb_learners(const cb_ctx* c);
+
+/* Algorithm 2 (Sec. 3.4), one observation for one GPU: l learners gave
+ * throughput t and t_prev was observed before.  Returns l + 1 if t - t_prev
+ * exceeds threshold (but at most l_max), l - 1 if t < t_prev (but at least
+ * one learner; the algorithm's guard "l > 0" is read as "l > 1"), else l.
+ * The caller keeps t as the next t_prev.  Pure host function. */
+int cb_tuner_next(int l, double t, double t_prev, double threshold, int l_max);
 
 /* --- operator test hooks ------------------------------------------------
  * One operator of the learning task on caller device buffers, through the

@@ -33,6 +33,7 @@ EXPORTS = (
     "cb_profile_enable", "cb_profile_collect", "cb_profile_entry", "cb_profile_clear",
     "cb_test_conv_scratch_bytes", "cb_test_conv", "cb_test_bn_scratch_bytes", "cb_test_bn_fwd",
     "cb_test_bn_bwd", "cb_test_maxpool", "cb_test_softmax_xent",
+    "cb_set_lr", "cb_restart", "cb_set_learners", "cb_learners", "cb_tuner_next",
 )
 
 
@@ -99,6 +100,11 @@ def lib():
                                                 _P, ctypes.c_size_t, _P]
         L.cb_test_maxpool.argtypes = [_i] * 7 + [_P, _P, _P, _P, _i, _P, _P]
         L.cb_test_softmax_xent.argtypes = [_i] * 3 + [_P, _P, _P, _P, _P]
+        L.cb_set_lr.argtypes = [_P, ctypes.c_float]
+        L.cb_restart.argtypes = [_P]
+        L.cb_set_learners.argtypes = [_P, _i, ctypes.c_float]
+        L.cb_learners.argtypes = [_P]
+        L.cb_tuner_next.argtypes = [_i, ctypes.c_double, ctypes.c_double, ctypes.c_double, _i]
         _lib = L
     return _lib
 
@@ -114,6 +120,11 @@ def cb_num_params(m: cb_model) -> int:
     if n < 0:
         raise CBError(n, "unsupported model")
     return int(n)
+
+
+def cb_tuner_next(l: int, t: float, t_prev: float, threshold: float, l_max: int) -> int:
+    """Algorithm 2, one observation (the library's decision rule)."""
+    return int(lib().cb_tuner_next(l, t, t_prev, threshold, l_max))
 
 
 def cb_tensor_layout(m: cb_model):
@@ -151,6 +162,7 @@ class Context:
 
         L = lib()
         self.m, self.k, self.b = m, k, b
+        self.capacity = k
         self.P = cb_num_params(m)
         w0 = _host_f32(w0)
         if w0.size != self.P:
@@ -195,6 +207,18 @@ class Context:
 
     def cb_wait(self):
         return self._check(lib().cb_wait(self._c), "cb_wait")
+
+    # -- control between iterations -----------------------------------------
+    def cb_set_lr(self, lr):
+        return self._check(lib().cb_set_lr(self._c, lr), "cb_set_lr")
+
+    def cb_restart(self):
+        return self._check(lib().cb_restart(self._c), "cb_restart")
+
+    def cb_set_learners(self, k, alpha):
+        self._check(lib().cb_set_learners(self._c, k, alpha), "cb_set_learners")
+        self.k = lib().cb_learners(self._c)
+        return 0
 
     def cb_get_central(self):
         out = np.empty(self.P, dtype=np.float32)

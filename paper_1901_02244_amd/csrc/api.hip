@@ -68,6 +68,7 @@ struct ParamInfo {
 struct Plan {
   cb_model m{};
   int k = 0, b = 0;
+  int kcap = 0;  // replicas the parameter state is laid out for (k <= kcap)
   std::vector<Tensor> t;
   std::vector<Op> ops;
   std::vector<ParamInfo> params;
@@ -254,13 +255,17 @@ ConvGeom geom(const Plan& p, const Op& o) {
   return g;
 }
 
-// Builds the operator list, the backward routing and the workspace layout.
-// Returns false for an unsupported model.
-bool make_plan(const cb_model* m, int k, int b, Plan& p) {
+// Builds the operator list, the backward routing and the workspace layout
+// for k active learners.  The parameter state (W, G, z, z_prev, w_prev)
+// comes first and is laid out for kcap replicas, so plans for any k <= kcap
+// put it at the same place.  Returns false for an unsupported model.
+bool make_plan(const cb_model* m, int k, int b, Plan& p, int kcap = 0) {
   p = Plan();
   if (!m || k < 1 || b < 1 || m->in_c < 1 || m->num_classes < 1) return false;
+  if (kcap < k) kcap = k;
   p.m = *m;
   p.k = k;
+  p.kcap = kcap;
   p.b = b;
   Builder B(p);
   p.input = B.tensor(m->in_c, m->in_h, m->in_w);
@@ -328,7 +333,7 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p) {
     off = align_up(off + bytes, ALIGN);
     return o;
   };
-  const int64_t kp = (int64_t)k * p.Pp * 4;
+  const int64_t kp = (int64_t)kcap * p.Pp * 4;
   p.off_W = take(kp);
   p.off_G = take(kp);
   p.off_Z = take(p.Pp * 4);
@@ -426,6 +431,7 @@ struct ProfAgg {
 struct cb_ctx {
   Plan p;
   char* ws = nullptr;
+  size_t ws_bytes = 0;
   hipStream_t stream = nullptr;
   int device = 0;
   float alpha = 0, lr = 0, mu = 0;
@@ -808,10 +814,42 @@ int cb_tensor_info(const cb_model* m, int idx, int64_t* offset, int* kind, int* 
   return CB_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// The split-reduction tables of the current plan (one segment per layer
+// whose weight gradient is split).
+void build_split_tables(cb_ctx* c) {
+  c->split_tables.clear();
+  c->split_bytes.clear();
+  for (const Op& o : c->p.ops) {
+    if (o.kind != OP_CONV || o.splits <= 1) continue;
+    if (c->split_tables.empty() || c->split_tables.back().nseg == MAX_SPLIT_SEGS) {
+      c->split_tables.emplace_back();
+      c->split_tables.back().pstride = c->p.Pp;
+      c->split_bytes.push_back(0.0);
+    }
+    const int64_t wn = (int64_t)o.Co * o.Ci * o.R * o.R;
+    split_table_add(c->split_tables.back(), c->at<float>(o.part_off), c->G() + o.w_off, wn,
+                    o.splits);
+    c->split_bytes.back() += 4.0 * c->p.k * wn * (o.splits + 1.0);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
 size_t cb_workspace_bytes(const cb_model* m, int k, int b) {
-  Plan p;
-  if (!make_plan(m, k, b, p)) return 0;
-  return (size_t)p.total;
+  // enough for every number of active learners up to k (cb_set_learners)
+  int64_t most = 0;
+  for (int kk = 1; kk <= k; ++kk) {
+    Plan p;
+    if (!make_plan(m, kk, b, p, k)) return 0;
+    most = std::max(most, p.total);
+  }
+  return (size_t)most;
 }
 
 int cb_create(const cb_model* m, int k, int b, float alpha, float lr, float momentum,
@@ -835,24 +873,14 @@ int cb_create(const cb_model* m, int k, int b, float alpha, float lr, float mome
     delete c;
     return fail(nullptr, CB_EINVAL, "workspace is NULL or not 256-byte aligned");
   }
-  if ((int64_t)ws_bytes < c->p.total) {
+  if (ws_bytes < cb_workspace_bytes(m, k, b)) {
     delete c;
     return fail(nullptr, CB_ENOMEM, "workspace smaller than cb_workspace_bytes()");
   }
   c->ws = static_cast<char*>(workspace_dev);
   c->stream = static_cast<hipStream_t>(hip_stream);
-  for (const Op& o : c->p.ops) {
-    if (o.kind != OP_CONV || o.splits <= 1) continue;
-    if (c->split_tables.empty() || c->split_tables.back().nseg == MAX_SPLIT_SEGS) {
-      c->split_tables.emplace_back();
-      c->split_tables.back().pstride = c->p.Pp;
-      c->split_bytes.push_back(0.0);
-    }
-    const int64_t wn = (int64_t)o.Co * o.Ci * o.R * o.R;
-    split_table_add(c->split_tables.back(), c->at<float>(o.part_off), c->G() + o.w_off, wn,
-                    o.splits);
-    c->split_bytes.back() += 4.0 * k * wn * (o.splits + 1.0);
-  }
+  c->ws_bytes = ws_bytes;
+  build_split_tables(c);
   c->alpha = alpha;
   c->lr = lr;
   c->mu = momentum;
@@ -995,6 +1023,65 @@ int cb_set_state(cb_ctx* c, const float* W_host, const float* z_host, const floa
   CB_HIP(c, hipStreamSynchronize(c->stream));
   c->pending = false;
   return CB_OK;
+}
+
+int cb_set_lr(cb_ctx* c, float lr) {
+  int rc = enter(c);
+  if (rc) return rc;
+  if (!std::isfinite(lr)) return fail(c, CB_EINVAL, "lr must be finite");
+  c->lr = lr;
+  return CB_OK;
+}
+
+int cb_restart(cb_ctx* c) {
+  int rc = enter(c);
+  if (rc) return rc;
+  const Plan& p = c->p;
+  const size_t pb = (size_t)p.P * 4;
+  for (int j = 0; j < p.k; ++j) {
+    CB_HIP(c, hipMemcpyAsync(c->W() + (int64_t)j * p.Pp, c->Z(), pb, hipMemcpyDeviceToDevice,
+                             c->stream));
+    if (c->Wprev())
+      CB_HIP(c, hipMemcpyAsync(c->Wprev() + (int64_t)j * p.Pp, c->Z(), pb,
+                               hipMemcpyDeviceToDevice, c->stream));
+  }
+  CB_HIP(c, hipMemcpyAsync(c->Zp(), c->Z(), pb, hipMemcpyDeviceToDevice, c->stream));
+  c->pending = false;
+  return CB_OK;
+}
+
+int cb_set_learners(cb_ctx* c, int k, float alpha) {
+  int rc = enter(c);
+  if (rc) return rc;
+  if (c->pending) return fail(c, CB_ESTATE, "cb_set_learners: a gradient is pending (sync first)");
+  if (k < 1 || k > c->p.kcap)
+    return fail(c, CB_EINVAL, "k must be between 1 and the capacity given to cb_create");
+  if (!std::isfinite(alpha)) return fail(c, CB_EINVAL, "alpha must be finite");
+  Plan np;
+  if (!make_plan(&c->p.m, k, c->p.b, np, c->p.kcap) || (size_t)np.total > c->ws_bytes ||
+      np.off_W != c->p.off_W || np.off_Z != c->p.off_Z)
+    return fail(c, CB_EINVAL, "cb_set_learners: no plan for this k in the workspace");
+  // new learners start from the latest central model, with zero velocity
+  const size_t pb = (size_t)c->p.P * 4;
+  for (int j = c->p.k; j < k; ++j) {
+    CB_HIP(c, hipMemcpyAsync(c->W() + (int64_t)j * c->p.Pp, c->Z(), pb,
+                             hipMemcpyDeviceToDevice, c->stream));
+    if (c->Wprev())
+      CB_HIP(c, hipMemcpyAsync(c->Wprev() + (int64_t)j * c->p.Pp, c->Z(), pb,
+                               hipMemcpyDeviceToDevice, c->stream));
+  }
+  c->p = std::move(np);
+  c->alpha = alpha;
+  build_split_tables(c);
+  return CB_OK;
+}
+
+int cb_learners(const cb_ctx* c) { return c ? c->p.k : CB_EINVAL; }
+
+int cb_tuner_next(int l, double t, double t_prev, double threshold, int l_max) {
+  if (t - t_prev > threshold) return l < l_max ? l + 1 : l;
+  if (t < t_prev && l > 1) return l - 1;
+  return l;
 }
 
 int cb_profile_enable(cb_ctx* c, int on) {

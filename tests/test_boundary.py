@@ -95,3 +95,21 @@ def test_create_validates_before_device_use():
     # calls on a NULL context are rejected
     assert L.cb_sync(None) == cb.CB_EINVAL
     assert L.cb_step(None, None, None) == cb.CB_EINVAL
+
+
+def test_tuner_rule_matches_oracle(oracle_lib):
+    """Algorithm 2's decision rule in the library (host code) against the
+    oracle's, on random throughput sequences: integer decisions, exact."""
+    import oracle
+    rng = np.random.default_rng(11)
+    for _ in range(200):
+        l_max = int(rng.integers(1, 40))
+        thr = float(rng.uniform(0, 50))
+        l_lib = l_ref = int(rng.integers(1, l_max + 1))
+        tp = 0.0
+        for t in rng.uniform(0, 1000, 30):
+            l_lib = cb.cb_tuner_next(l_lib, float(t), tp, thr, l_max)
+            l_ref = oracle.tuner_next(l_ref, float(t), tp, thr, l_max)
+            assert l_lib == l_ref
+            assert 1 <= l_lib <= l_max
+            tp = float(t)

@@ -197,6 +197,73 @@ def test_lenet_learner_momentum_and_unsynced_steps():
     p.check_state(tol=TOL_AMBIGUOUS)
 
 
+def test_control_between_iterations():
+    """Learner resizing (Sec. 3.4), a learning-rate change and a restart
+    (Sec. 3.2) between iterations, on the GPU and in the oracle: a LeNet job
+    with capacity 4 goes 2 -> 3 -> 1 -> 4 learners.  New replicas start
+    bitwise at z, a restart puts every replica and z_prev bitwise at z, and
+    the state tracks the oracle after every phase."""
+    p = Pair("lenet5", 1, 28, 28, 10, k=4, b=5, seed=5)
+    t = 0
+
+    def run(n):
+        nonlocal t
+        for _ in range(n):
+            p.step(t)
+            p.sync()
+            t += 1
+
+    def resize(k):
+        p.gpu.cb_set_learners(k, 1.0 / k)
+        assert p.ref.set_learners(k, f32(1.0 / k)) == 0
+        p.k = k
+
+    resize(2)
+    run(2)
+    p.check_state(tol=TOL_AMBIGUOUS)
+    z = p.gpu.cb_get_central()
+    resize(3)
+    np.testing.assert_array_equal(p.gpu.cb_get_replica(2), z)
+    run(2)
+    p.check_state(tol=TOL_AMBIGUOUS)
+    p.gpu.cb_set_lr(0.03)
+    p.ref.set_lr(f32(0.03))
+    run(1)
+    p.check_state(tol=TOL_AMBIGUOUS)
+    p.gpu.cb_restart()
+    p.ref.restart()
+    z = p.gpu.cb_get_central()
+    np.testing.assert_array_equal(p.gpu.cb_get_prev_central(), z)
+    for j in range(3):
+        np.testing.assert_array_equal(p.gpu.cb_get_replica(j), z)
+    run(1)
+    resize(1)
+    run(1)
+    resize(4)
+    run(1)
+    p.check_state(tol=TOL_AMBIGUOUS)
+    assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
+    # resizing needs an iteration barrier, and the capacity bounds k
+    p.step(t)
+    with pytest.raises(cb.CBError):
+        p.gpu.cb_set_learners(2, 0.5)
+    p.sync()
+    with pytest.raises(cb.CBError):
+        p.gpu.cb_set_learners(5, 0.2)
+
+
+def test_ea_sgd_mode_and_sync_interval():
+    """mu = 0 (synchronous elastic averaging, the comparison of Sec. 5.5)
+    with a sync interval of 3: two local steps, then a synchronisation."""
+    p = Pair("lenet5", 1, 28, 28, 10, k=3, b=5, mu=0.0, seed=5)
+    for t in range(6):
+        p.step(t)
+        if t % 3 == 2:
+            p.sync()
+    p.check_state(tol=TOL_AMBIGUOUS)
+    assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
+
+
 def test_resnet32_ragged_batch():
     """Every ResNet-32 path (stride-2 option-A blocks, BN, average pool) with
     3 images per learner: partial tiles in every GEMM; 16x16 images and a
