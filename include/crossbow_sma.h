@@ -233,6 +233,26 @@ int cb_test_maxpool(int N, int C, int H, int W, int K, int stride, int pad, cons
                     float* y, const float* dy, float* dx, int mask_relu, int* arg_scratch,
                     void* stream);
 
+/* The data gradient of one convolution with every operand its fused
+ * epilogue can take, as cb_step uses it: dx = conv_bwd(dy) (+ dx if
+ * accumulate) (+ add: ADD_SAME = 1, same shape as dx; ADD_SUBSAMPLE = 2,
+ * add is [k*b][add_C][Ho][Wo] and reaches the pixels whose row and column are
+ * multiples of stride, channel by channel), zeroed where mask <= 0 (mask
+ * may be NULL); then, if bn_part is not NULL, dx is the output gradient of
+ * a batch norm with input bn_x and statistics bn_mean / bn_istd [k][Ci]:
+ * with d = dx where bn_y > 0 (all of dx if bn_y is NULL) and
+ * xh = (bn_x - mean) * istd, per replica and channel the partial sums of d
+ * and d*xh are written to bn_part [k][Ci][parts][2] (fp64), parts =
+ * cb_test_conv_dgrad_parts(); their sum over parts is the total.  Same
+ * kernels and tile choices as cb_step; device pointers 16-byte aligned. */
+int cb_test_conv_dgrad_parts(int k, int b, int Ci, int H, int W, int Co, int R, int stride,
+                             int pad);
+int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int stride, int pad,
+                       const float* dy, const float* params, int64_t pstride, float* dx,
+                       int accumulate, const float* mask, const float* add, int add_mode,
+                       int add_C, const float* bn_x, const float* bn_y, const float* bn_mean,
+                       const float* bn_istd, double* bn_part, void* stream);
+
 /* Mean softmax cross-entropy of each replica's b rows of logits (Eq. 2),
  * loss [k], and its gradient dlogits [k*b][classes]. */
 int cb_test_softmax_xent(int k, int b, int classes, const float* logits, const int32_t* labels,

@@ -34,6 +34,7 @@ EXPORTS = (
     "cb_test_conv_scratch_bytes", "cb_test_conv", "cb_test_bn_scratch_bytes", "cb_test_bn_fwd",
     "cb_test_bn_bwd", "cb_test_maxpool", "cb_test_softmax_xent",
     "cb_set_lr", "cb_restart", "cb_set_learners", "cb_learners", "cb_tuner_next",
+    "cb_test_conv_dgrad_parts", "cb_test_conv_dgrad",
 )
 
 
@@ -100,6 +101,9 @@ def lib():
                                                 _P, ctypes.c_size_t, _P]
         L.cb_test_maxpool.argtypes = [_i] * 7 + [_P, _P, _P, _P, _i, _P, _P]
         L.cb_test_softmax_xent.argtypes = [_i] * 3 + [_P, _P, _P, _P, _P]
+        L.cb_test_conv_dgrad_parts.argtypes = [_i] * 9
+        L.cb_test_conv_dgrad.argtypes = [_i] * 9 + [_P, _P, ctypes.c_int64, _P, _i, _P, _P, _i, _i,
+                                                    _P, _P, _P, _P, _P, _P]
         L.cb_set_lr.argtypes = [_P, ctypes.c_float]
         L.cb_restart.argtypes = [_P]
         L.cb_set_learners.argtypes = [_P, _i, ctypes.c_float]

@@ -182,26 +182,31 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   const int wbase = FLIP ? kq * WS + (lane & 15) * 9 : (lane & 15) * WS + kq * 9;
 
   // Epilogue operands of the data gradient (ReLU mask, the next batch
-  // norm's x and y), loaded before the tile's last MFMAs so their latency
-  // overlaps the contraction: four consecutive pixels of one channel per
-  // lane and block.
-  v4f e_mask[TM][TN], e_x[TM][TN], e_y[TM][TN];
+  // norm's x and y), loaded together with the inputs of the tile before, so
+  // their latency overlaps a whole tile: four consecutive pixels of one
+  // channel per lane and block.
+  // With 32-channel tiles a second set does not fit in the registers: those
+  // load the operands just before the tile's last MFMAs instead.
+  constexpr bool AHEAD = FLIP && TN == 1;
+  v4f e_mask[TM][TN], e_x[TM][TN], e_y[TM][TN];     // this tile's
+  v4f n_mask[TM][TN], n_x[TM][TN], n_y[TM][TN];     // the next tile's (AHEAD)
   auto gofs = [&](const Tile& d, int t, int u) {  // (plane offset, first pixel)
     const int co = d.co0 + u * 16 + (lane & 15);
     const int p0 = d.oh0 * WW + (wave * TM + t) * 16 + 4 * kq;
     return (int64_t)((d.j * a.b + d.img) * a.Cout + co) * HW + p0;
   };
-  auto prefetch_epilogue = [&](const Tile& d) {
+  auto prefetch_epilogue = [&](const Tile& d, v4f (&m)[TM][TN], v4f (&x)[TM][TN],
+                               v4f (&y)[TM][TN]) {
     if (!FLIP) return;
 #pragma unroll
     for (int t = 0; t < TM; ++t)
 #pragma unroll
       for (int u = 0; u < TN; ++u) {
         const int64_t g = gofs(d, t, u);
-        if (a.mask) e_mask[t][u] = *reinterpret_cast<const v4f*>(a.mask + g);
+        if (a.mask) m[t][u] = *reinterpret_cast<const v4f*>(a.mask + g);
         if (a.bn_part) {
-          e_x[t][u] = *reinterpret_cast<const v4f*>(a.bn_x + g);
-          if (a.bn_y) e_y[t][u] = *reinterpret_cast<const v4f*>(a.bn_y + g);
+          x[t][u] = *reinterpret_cast<const v4f*>(a.bn_x + g);
+          if (a.bn_y) y[t][u] = *reinterpret_cast<const v4f*>(a.bn_y + g);
         }
       }
   };
@@ -247,8 +252,8 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
             for (int i = 0; i < 4; ++i) {
               const int p = p0 + i, ih = p / WW, iw = p - ih * WW;
               if (ih % st == 0 && iw % st == 0)
-                v[i] += a.add[(((int64_t)(d.j * a.b + d.img) * a.add_C + co) * (H / st) + ih / st) *
-                                  (WW / st) + iw / st];
+                v[i] += a.add[(((int64_t)(d.j * a.b + d.img) * a.add_C + co) * ((H + st - 1) / st) +
+                               ih / st) * ((WW + st - 1) / st) + iw / st];
             }
           }
           if (a.mask)
@@ -301,6 +306,7 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   int t = blockIdx.x;
   Tile d = decode(t);
   load(d, 0);
+  if (AHEAD) prefetch_epilogue(d, e_mask, e_x, e_y);
   store(0);
   __syncthreads();
   int cur = 0;
@@ -315,7 +321,10 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       const bool last = c + 1 == nchunk;
       const bool has_next = !last || more;
       if (has_next) load(last ? dn : d, last ? 0 : (c + 1) * CC);
-      if (last) prefetch_epilogue(d);
+      // the next tile's epilogue operands go out with its inputs, a whole
+      // tile ahead of their use
+      if (AHEAD && last && more) prefetch_epilogue(dn, n_mask, n_x, n_y);
+      if (!AHEAD && last) prefetch_epilogue(d, e_mask, e_x, e_y);
       const float* X = xs[cur];
       const float* Wl = ws[cur];
 #pragma unroll TAP_UNROLL
@@ -337,6 +346,288 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
         }
       }
       if (has_next) store(cur ^ 1);
+      __syncthreads();
+      cur ^= 1;
+    }
+    epilogue(d);
+    if (!more) break;
+    t += G;
+    d = dn;
+    if (AHEAD) {
+#pragma unroll
+      for (int x = 0; x < TM; ++x)
+#pragma unroll
+        for (int y = 0; y < TN; ++y) {
+          e_mask[x][y] = n_mask[x][y];
+          e_x[x][y] = n_x[x][y];
+          e_y[x][y] = n_y[x][y];
+        }
+    }
+  }
+}
+
+// Data gradient of a 3x3, stride 2, pad 1 convolution, by output parity.
+// dX[ci][ih][iw] = sum over co and the taps (r, s) with ih + 1 - r and
+// iw + 1 - s even of W[co][ci][r][s] dY[co][(ih + 1 - r) / 2][(iw + 1 - s) / 2].
+// Split dX by (ih % 2, iw % 2) = (ph, pw): each class is a stride-1
+// convolution on the dY grid, class pixel (m, n) = dX pixel (2m+ph, 2n+pw),
+// over the taps r in {1} (ph = 0) or {0, 2} (ph = 1), likewise s, reading dY
+// at (m + (ph + 1 - r) / 2, n + (pw + 1 - s) / 2) -- 9 taps over the four
+// classes instead of the 4 x 9 of a zero-filled implicit GEMM.  A
+// workgroup computes all four classes of THO dY rows (2*THO dX rows) for BN
+// dX channels from one dY tile in LDS (rows m0 .. m0+THO, columns 0 .. WO,
+// zero beyond the image).  MFMA rows are 16 consecutive class pixels, so
+// a lane holds the pw = 0 and pw = 1 values of the same four positions:
+// 8 consecutive dX pixels, moved as two float4s in the epilogue.
+template <int WO, int THO, int BN, int CC>
+__global__ __launch_bounds__(256) void conv3x3s2_dgrad_k(DirectArgs a) {
+  constexpr int WPo = WO + 1, HRo = THO + 1;
+  constexpr int CS = pad_cs(HRo * WPo);
+  constexpr int MC = THO * WO;            // pixels of one class per tile
+  constexpr int TM = MC / 64;             // 16-pixel blocks per wave and class
+  constexpr int TN = BN / 16;
+  constexpr int WS = BN == 16 ? 144 : 304;  // filter rows: contraction channel
+  constexpr int WRUN = BN * 9;
+  constexpr int NX = CC * HRo * WPo, NXT = (NX + 255) / 256;
+  constexpr int NW = CC * WRUN, NWT = (NW + 255) / 256;
+  static_assert(TM >= 1 && MC % 64 == 0, "class tile must cover whole 64-pixel wave strips");
+  __shared__ __attribute__((aligned(16))) float xs[2][CC * CS];
+  __shared__ __attribute__((aligned(16))) float ws[2][CC * WS];
+  __shared__ double red[4][BN][2];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4;
+  const int l16 = lane & 15;
+  const int HO = a.H / 2, W = 2 * WO, HW = a.H * W, HWo = HO * WO;
+  const int tiles_img = HO / THO;
+  const int rows_rep = a.b * tiles_img;
+  const int per_rep = rows_rep * (a.Cout / BN);
+  const int T = a.k * per_rep;
+  const int nchunk = a.Cin / CC;
+
+  struct Tile {
+    int j, co0, rt, img, m0;
+  };
+  auto decode = [&](int t) {
+    Tile d;
+    d.j = t / per_rep;
+    const int r = t - d.j * per_rep;
+    const int ct = r / rows_rep;
+    d.rt = r - ct * rows_rep;
+    d.co0 = ct * BN;  // first dX channel of the tile
+    d.img = d.rt / tiles_img;
+    d.m0 = (d.rt - d.img * tiles_img) * THO;
+    return d;
+  };
+
+  float rx[NXT], rw[NWT];
+  auto load = [&](const Tile& d, int c0) {
+    const float* DY = a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HWo;
+    const float* Wt = a.w + (int64_t)d.j * a.pstride;
+#pragma unroll
+    for (int u = 0; u < NXT; ++u) {
+      const int e = tid + u * 256;
+      float v = 0.f;
+      if (e < NX) {
+        const int c = e / (HRo * WPo), rem = e - c * (HRo * WPo), hr = rem / WPo, wc = rem - hr * WPo;
+        const int m = d.m0 + hr;
+        if (m < HO && wc < WO) v = DY[(int64_t)(c0 + c) * HWo + m * WO + wc];
+      }
+      rx[u] = v;
+    }
+#pragma unroll
+    for (int u = 0; u < NWT; ++u) {
+      // the filter [co][ci][tap] of the convolution: rows co = c0 + row (the
+      // contraction), runs over ci in the tile and the taps
+      const int e = tid + u * 256;
+      float v = 0.f;
+      if (e < NW) {
+        const int row = e / WRUN, rem = e - row * WRUN;
+        v = Wt[((int64_t)(c0 + row) * a.Cout + d.co0) * 9 + rem];
+      }
+      rw[u] = v;
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < NXT; ++u) {
+      const int e = tid + u * 256;
+      if (e < NX) {
+        const int c = e / (HRo * WPo);
+        xs[buf][c * CS + e - c * (HRo * WPo)] = rx[u];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NWT; ++u) {
+      const int e = tid + u * 256;
+      if (e < NW) {
+        const int row = e / WRUN;
+        ws[buf][row * WS + e - row * WRUN] = rw[u];
+      }
+    }
+  };
+
+  // lane pixel of each 16-pixel class block: (mloc, n)
+  int xbase[TM];
+#pragma unroll
+  for (int t = 0; t < TM; ++t) {
+    const int m = (wave * TM + t) * 16 + l16;
+    const int ml = m / WO, n = m - ml * WO;
+    xbase[t] = kq * CS + ml * WPo + n;
+  }
+  const int wbase = kq * WS + l16 * 9;
+
+  // acc[ph][pw][t][u]
+  v4f acc[2][2][TM][TN];
+
+  auto epilogue = [&](const Tile& d) {
+    const int n_img = d.j * a.b + d.img;
+    double s1[TN], s2[TN];
+#pragma unroll
+    for (int u = 0; u < TN; ++u) s1[u] = s2[u] = 0.0;
+#pragma unroll
+    for (int u = 0; u < TN; ++u) {
+      const int ci = d.co0 + u * 16 + l16;
+      float bm = 0.f, bi = 0.f;
+      if (a.bn_part) {
+        bm = a.bn_mean[d.j * a.Cout + ci];
+        bi = a.bn_istd[d.j * a.Cout + ci];
+      }
+#pragma unroll
+      for (int t = 0; t < TM; ++t) {
+        const int mp = (wave * TM + t) * 16 + 4 * kq;  // first of the lane's 4 class pixels
+        const int ml = mp / WO, n = mp - ml * WO;
+#pragma unroll
+        for (int ph = 0; ph < 2; ++ph) {
+          const int ih = 2 * (d.m0 + ml) + ph;
+          const int64_t idx = ((int64_t)n_img * a.Cout + ci) * HW + ih * W + 2 * n;
+          // dX pixels 2n .. 2n+7 of row ih: even columns from class pw = 0
+          v4f lo, hi;
+          lo[0] = acc[ph][0][t][u][0]; lo[1] = acc[ph][1][t][u][0];
+          lo[2] = acc[ph][0][t][u][1]; lo[3] = acc[ph][1][t][u][1];
+          hi[0] = acc[ph][0][t][u][2]; hi[1] = acc[ph][1][t][u][2];
+          hi[2] = acc[ph][0][t][u][3]; hi[3] = acc[ph][1][t][u][3];
+          if (a.accumulate) {
+            lo += *reinterpret_cast<const v4f*>(a.out + idx);
+            hi += *reinterpret_cast<const v4f*>(a.out + idx + 4);
+          }
+          if (a.add_mode == ADD_SAME) {
+            lo += *reinterpret_cast<const v4f*>(a.add + idx);
+            hi += *reinterpret_cast<const v4f*>(a.add + idx + 4);
+          } else if (a.add_mode == ADD_SUBSAMPLE && a.add_st == 2 && ph == 0) {
+            // even rows and columns take src[n][ci][ih/2][iw/2]: the four
+            // class positions (m, n .. n+3)
+            const v4f sv = *reinterpret_cast<const v4f*>(
+                a.add + (((int64_t)n_img * a.add_C + ci) * HO + d.m0 + ml) * WO + n);
+            lo[0] += sv[0]; lo[2] += sv[1]; hi[0] += sv[2]; hi[2] += sv[3];
+          }
+          if (a.mask) {
+            const v4f m0 = *reinterpret_cast<const v4f*>(a.mask + idx);
+            const v4f m1 = *reinterpret_cast<const v4f*>(a.mask + idx + 4);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              if (!(m0[i] > 0.f)) lo[i] = 0.f;
+              if (!(m1[i] > 0.f)) hi[i] = 0.f;
+            }
+          }
+          *reinterpret_cast<v4f*>(a.out + idx) = lo;
+          *reinterpret_cast<v4f*>(a.out + idx + 4) = hi;
+          if (a.bn_part) {
+            const v4f x0 = *reinterpret_cast<const v4f*>(a.bn_x + idx);
+            const v4f x1 = *reinterpret_cast<const v4f*>(a.bn_x + idx + 4);
+            v4f y0 = v4f{1.f, 1.f, 1.f, 1.f}, y1 = y0;
+            if (a.bn_y) {
+              y0 = *reinterpret_cast<const v4f*>(a.bn_y + idx);
+              y1 = *reinterpret_cast<const v4f*>(a.bn_y + idx + 4);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float d0 = y0[i] > 0.f ? lo[i] : 0.f;
+              s1[u] += (double)d0;
+              s2[u] += (double)d0 * ((x0[i] - bm) * bi);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float d1 = y1[i] > 0.f ? hi[i] : 0.f;
+              s1[u] += (double)d1;
+              s2[u] += (double)d1 * ((x1[i] - bm) * bi);
+            }
+          }
+        }
+      }
+    }
+    if (!a.bn_part) return;
+#pragma unroll
+    for (int u = 0; u < TN; ++u) {
+      double x = s1[u], y = s2[u];
+      x += shfl_xor_d(x, 16);
+      y += shfl_xor_d(y, 16);
+      x += shfl_xor_d(x, 32);
+      y += shfl_xor_d(y, 32);
+      if (lane < 16) {
+        red[wave][u * 16 + lane][0] = x;
+        red[wave][u * 16 + lane][1] = y;
+      }
+    }
+    __syncthreads();
+    if (tid < BN) {
+      const double x = ((red[0][tid][0] + red[1][tid][0]) + red[2][tid][0]) + red[3][tid][0];
+      const double y = ((red[0][tid][1] + red[1][tid][1]) + red[2][tid][1]) + red[3][tid][1];
+      double* o = a.bn_part + (((int64_t)d.j * a.Cout + d.co0 + tid) * rows_rep + d.rt) * 2;
+      o[0] = x;
+      o[1] = y;
+    }
+  };
+
+  const int G = gridDim.x;
+  int t = blockIdx.x;
+  Tile d = decode(t);
+  load(d, 0);
+  store(0);
+  __syncthreads();
+  int cur = 0;
+  while (true) {
+#pragma unroll
+    for (int ph = 0; ph < 2; ++ph)
+#pragma unroll
+      for (int pw = 0; pw < 2; ++pw)
+#pragma unroll
+        for (int x = 0; x < TM; ++x)
+#pragma unroll
+          for (int y = 0; y < TN; ++y) acc[ph][pw][x][y] = v4f{0.f, 0.f, 0.f, 0.f};
+    const bool more = t + G < T;
+    const Tile dn = more ? decode(t + G) : d;
+    for (int c = 0; c < nchunk; ++c) {
+      const bool last = c + 1 == nchunk;
+      if (!last || more) load(last ? dn : d, last ? 0 : (c + 1) * CC);
+      const float* X = xs[cur];
+      const float* Wl = ws[cur];
+#pragma unroll
+      for (int ph = 0; ph < 2; ++ph)
+#pragma unroll
+        for (int pw = 0; pw < 2; ++pw)
+#pragma unroll
+          for (int ir = 0; ir < 1 + ph; ++ir)
+#pragma unroll
+            for (int is = 0; is < 1 + pw; ++is) {
+              // taps of the class: r = 1 (ph = 0) or r in {0, 2} (ph = 1)
+              const int r = ph ? 2 * ir : 1, s = pw ? 2 * is : 1;
+              const int dr = (ph + 1 - r) / 2, ds = (pw + 1 - s) / 2;
+              const int tap = r * 3 + s;
+#pragma unroll
+              for (int cg = 0; cg < CC / 4; ++cg) {
+                float av[TM], bv[TN];
+#pragma unroll
+                for (int x = 0; x < TM; ++x) av[x] = X[xbase[x] + cg * 4 * CS + dr * WPo + ds];
+#pragma unroll
+                for (int u = 0; u < TN; ++u) bv[u] = Wl[wbase + cg * 4 * WS + u * 144 + tap];
+#pragma unroll
+                for (int x = 0; x < TM; ++x)
+#pragma unroll
+                  for (int u = 0; u < TN; ++u)
+                    acc[ph][pw][x][u] = mfma4(av[x], bv[u], acc[ph][pw][x][u]);
+              }
+            }
+      if (!last || more) store(cur ^ 1);
       __syncthreads();
       cur ^= 1;
     }
@@ -495,6 +786,31 @@ hipError_t launch_wgrad(const WgradArgs& a, hipStream_t s, const char** name) {
   return hipGetLastError();
 }
 
+template <int WO, int THO, int BN, int CC>
+hipError_t launch_s2(const DirectArgs& a, hipStream_t s, const char** name) {
+  static int resident = 0;
+  if (!resident) {
+    int per_cu = 0, cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv3x3s2_dgrad_k<WO, THO, BN, CC>,
+                                                     256, 0) != hipSuccess)
+      return hipErrorInvalidValue;
+    resident = std::max(1, per_cu) * std::max(1, cus);
+  }
+  const int64_t T = (int64_t)a.k * a.b * (a.H / 2 / THO) * (a.Cout / BN);
+  const int64_t per = (T + resident - 1) / resident;
+  const int64_t G = (T + per - 1) / per;
+  klaunch(conv3x3s2_dgrad_k<WO, THO, BN, CC>, dim3((unsigned)G), dim3(256), 0, s, a);
+  if (name) {
+    static const std::string n = std::string("conv3x3s2_dgrad_k<") + std::to_string(WO) + ", " +
+                                 std::to_string(THO) + ", " + std::to_string(BN) + ", " +
+                                 std::to_string(CC) + ">";
+    *name = n.c_str();
+  }
+  return hipGetLastError();
+}
+
 template <int WW, int TH, int BN, int CC, bool FLIP>
 const char* direct_name() {
   static const std::string n = std::string("conv3x3_k<") + std::to_string(WW) + ", " +
@@ -583,6 +899,31 @@ void wgrad_split(const ConvGeom& g, int* splits, int* per) {
 }
 
 }  // namespace
+
+// Stride-2 data gradient: dY widths 8 and 16 (dX 16 and 32), channel
+// counts multiples of 16; THO dY rows per tile (64 class pixels).
+int s2_tho(int WO) { return WO == 16 ? 4 : 8; }
+
+bool conv_s2_dgrad_ok(const ConvGeom& g) {
+  return g.R == 3 && g.S == 3 && g.st == 2 && g.pad == 1 && g.H == g.W && g.H % 2 == 0 &&
+         (g.W == 16 || g.W == 32) && g.Ho == g.H / 2 && g.Ci % 16 == 0 && g.Co % 16 == 0;
+}
+
+int conv_s2_dgrad_tiles(const ConvGeom& g) { return g.b * (g.Ho / s2_tho(g.Wo)); }
+
+hipError_t conv_s2_dgrad(const ConvBwdDataArgs& d, hipStream_t s, const char** name) {
+  DirectArgs a{};
+  a.k = d.g.k; a.b = d.g.b; a.H = d.g.H;
+  a.Cin = d.g.Co; a.Cout = d.g.Ci;
+  a.in = d.dy; a.w = d.w; a.pstride = d.pstride; a.out = d.dx;
+  a.accumulate = d.accumulate; a.mask = d.mask;
+  a.add = d.add; a.add_mode = d.add_mode; a.add_C = d.add_C; a.add_st = d.add_st;
+  a.bn_part = d.bn_part; a.bn_x = d.bn_x; a.bn_y = d.bn_y;
+  a.bn_mean = d.bn_mean; a.bn_istd = d.bn_istd;
+  if (a.add_mode == ADD_SUBSAMPLE && a.add_st != 2) return hipErrorInvalidValue;
+  if (d.g.Wo == 16) return launch_s2<16, 4, 16, 16>(a, s, name);
+  return launch_s2<8, 8, 16, 16>(a, s, name);
+}
 
 bool conv_direct_wgrad_ok(const ConvGeom& g) {
   return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad);

@@ -329,7 +329,9 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
 
   float* DX = a.dx + (int64_t)j * g.b * N * HW;
   const float* MSK = a.mask ? a.mask + (int64_t)j * g.b * N * HW : nullptr;
-  const int Hs = g.H / (a.add_st > 0 ? a.add_st : 1), Ws = g.W / (a.add_st > 0 ? a.add_st : 1);
+  // the subsampled source keeps every st-th row and column: ceil(H / st) x ceil(W / st)
+  const int sst = a.add_st > 0 ? a.add_st : 1;
+  const int Hs = (g.H + sst - 1) / sst, Ws = (g.W + sst - 1) / sst;
   const float* ADD = a.add;
   if (ADD)
     ADD += (a.add_mode == ADD_SAME) ? (int64_t)j * g.b * N * HW
@@ -701,6 +703,7 @@ int conv_fwd_tiles_m(const ConvGeom& g) {
 
 int conv_bwd_data_tiles_m(const ConvGeom& g) {
   if (conv_direct_bwd_data_ok(g)) return conv_direct_bwd_data_tiles(g);
+  if (conv_s2_dgrad_ok(g)) return conv_s2_dgrad_tiles(g);
   const int64_t M = (int64_t)g.b * g.H * g.W;
   return (int)cdiv(M, tile_rows(pick_tile(M, g.Ci, g.k)));
 }
@@ -742,9 +745,10 @@ hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
 }
 
 hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
-  if (conv_direct_bwd_data_ok(a.g) && al16(a.dx) && al16(a.mask) && al16(a.bn_x) &&
-      al16(a.bn_y) && (a.add_mode != ADD_SAME || al16(a.add)))
-    return conv_direct_bwd_data(a, s, name);
+  const bool vec_ok = al16(a.dx) && al16(a.mask) && al16(a.bn_x) && al16(a.bn_y) && al16(a.add);
+  if (conv_direct_bwd_data_ok(a.g) && vec_ok) return conv_direct_bwd_data(a, s, name);
+  if (conv_s2_dgrad_ok(a.g) && vec_ok && (a.add_mode != ADD_SUBSAMPLE || a.add_st == 2))
+    return conv_s2_dgrad(a, s, name);
   const int key = a.g.R * 10 + a.g.st;
   switch (key) {
     case 11: return bwd_data_r<1, 1>(a, s, name);

@@ -55,8 +55,8 @@ struct ConvFwdArgs {
 
 // Residual added to a data gradient (the shortcut of a residual block):
 //   ADD_SAME: add src at the same index;
-//   ADD_SUBSAMPLE: src is [k*b][Csrc][H/st][W/st]; dX[n][c][h][w] gets
-//     src[n][c][h/st][w/st] when h and w are multiples of st (option-A
+//   ADD_SUBSAMPLE: src is [k*b][Csrc][ceil(H/st)][ceil(W/st)]; dX[n][c][h][w]
+//     gets src[n][c][h/st][w/st] when h and w are multiples of st (option-A
 //     shortcut read backwards; c < Ci <= Csrc).
 enum { ADD_NONE = 0, ADD_SAME = 1, ADD_SUBSAMPLE = 2 };
 
@@ -116,6 +116,12 @@ bool conv_direct_fwd_ok(const ConvGeom& g);
 bool conv_direct_bwd_data_ok(const ConvGeom& g);
 int conv_direct_fwd_tiles(const ConvGeom& g);
 int conv_direct_bwd_data_tiles(const ConvGeom& g);
+// 3x3 stride-2 pad-1 data gradients (dX 16 or 32 wide, channel counts
+// multiples of 16) run on a kernel that splits dX by pixel parity
+// (conv_bwd_data routes; *_tiles as above).
+bool conv_s2_dgrad_ok(const ConvGeom& g);
+int conv_s2_dgrad_tiles(const ConvGeom& g);
+hipError_t conv_s2_dgrad(const ConvBwdDataArgs& d, hipStream_t s, const char** name = nullptr);
 // Their weight gradient has a direct kernel too (conv_bwd_weight routes;
 // conv_bwd_weight_splits reports its split).
 bool conv_direct_wgrad_ok(const ConvGeom& g);

@@ -107,6 +107,42 @@ int cb_test_conv(int k, int b, int Ci, int H, int W, int Co, int R, int stride, 
   return rc_of(conv_bwd_data(d, s));
 }
 
+int cb_test_conv_dgrad_parts(int k, int b, int Ci, int H, int W, int Co, int R, int stride,
+                             int pad) {
+  if (!geom_ok(k, b, Ci, H, W, Co, R, stride, pad) || !conv_supported(R, R, stride, true))
+    return CB_EINVAL;
+  return conv_bwd_data_tiles_m(make_geom(k, b, Ci, H, W, Co, R, stride, pad));
+}
+
+int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int stride, int pad,
+                       const float* dy, const float* params, int64_t pstride, float* dx,
+                       int accumulate, const float* mask, const float* add, int add_mode,
+                       int add_C, const float* bn_x, const float* bn_y, const float* bn_mean,
+                       const float* bn_istd, double* bn_part, void* stream) {
+  if (!geom_ok(k, b, Ci, H, W, Co, R, stride, pad) || !conv_supported(R, R, stride, true) ||
+      !dy || !params || !dx || add_mode < ADD_NONE || add_mode > ADD_SUBSAMPLE ||
+      (add_mode != ADD_NONE && !add) || (bn_part && (!bn_x || !bn_mean || !bn_istd)))
+    return CB_EINVAL;
+  ConvBwdDataArgs d;
+  d.g = make_geom(k, b, Ci, H, W, Co, R, stride, pad);
+  d.dy = dy;
+  d.w = params;
+  d.pstride = pstride;
+  d.dx = dx;
+  d.accumulate = accumulate;
+  d.mask = mask;
+  d.add = add;
+  d.add_mode = add_mode;
+  d.add_C = add_C;
+  d.add_st = stride;
+  d.bn_part = bn_part;
+  d.bn_x = bn_x;
+  d.bn_y = bn_y;
+  d.bn_mean = bn_mean;
+  d.bn_istd = bn_istd;
+  return rc_of(conv_bwd_data(d, static_cast<hipStream_t>(stream)));
+}
+
 size_t cb_test_bn_scratch_bytes(int k, int b, int C, int H, int W) {
   if (k < 1 || b < 1 || C < 1 || H < 1 || W < 1) return 0;
   return (size_t)k * C * bn_chunks(b, H * W, C, k) * 2 * sizeof(double);

@@ -61,6 +61,10 @@ CONV = [
     ("direct.w16.k32", 32, 16, 32, 16, 32, 3, 1, 1, 0, 0, 1),
     ("direct.w8.32to64", 1, 16, 32, 8, 64, 3, 1, 1, 0, 1, 1),
     ("direct.w8.k32", 32, 16, 64, 8, 64, 3, 1, 1, 0, 0, 1),
+    # 3x3 stride-2 data gradients by pixel parity
+    ("s2.w32.k1", 1, 16, 16, 32, 32, 3, 2, 1, 0, 0, 1),
+    ("s2.w16.c48", 3, 2, 48, 16, 32, 3, 2, 1, 1, 1, 1),
+    ("s2.w16.k32", 32, 16, 32, 16, 64, 3, 2, 1, 0, 0, 1),
     # ragged: partial tiles in every GEMM dimension
     ("ragged.3x3s2", 3, 5, 7, 13, 19, 3, 2, 1, 0, 0, 1),
     ("ragged.5x5", 2, 3, 5, 11, 37, 5, 1, 2, 1, 1, 1),
@@ -276,3 +280,83 @@ def test_softmax_xent_kernel(case):
         lo, do = oracle.softmax_xent(o[j * b:(j + 1) * b], y[j * b:(j + 1) * b])
         assert abs(loss[j] - lo) / abs(lo) <= TOL_STEP1
         assert max_rel(d[j * b:(j + 1) * b], do) <= TOL_STEP1
+
+
+# (name, k, b, Ci, H, Co, R, stride, pad, accumulate, mask, add_mode, add_C, bn, bn_y)
+DGRAD_EPILOGUE = [
+    ("direct.w32.same.bn", 2, 4, 16, 32, 16, 3, 1, 1, 1, 1, 1, 16, 1, 1),
+    ("direct.w16.bn", 2, 3, 32, 16, 32, 3, 1, 1, 0, 0, 0, 0, 1, 1),
+    ("direct.w8.acc.mask", 2, 4, 64, 8, 64, 3, 1, 1, 1, 1, 1, 64, 1, 0),
+    ("s2.w32.sub.bn", 2, 4, 16, 32, 32, 3, 2, 1, 0, 0, 2, 32, 1, 1),
+    ("s2.w16.acc.mask.sub.bn", 2, 4, 32, 16, 64, 3, 2, 1, 1, 1, 2, 64, 1, 0),
+    ("s2.w16.same", 1, 3, 16, 16, 32, 3, 2, 1, 0, 1, 1, 16, 0, 0),
+    ("gemm.3x3s2.ragged.sub.bn", 2, 3, 7, 13, 19, 3, 2, 1, 1, 1, 2, 19, 1, 1),
+    ("gemm.5x5.mask", 2, 4, 6, 14, 16, 5, 1, 0, 0, 1, 0, 0, 1, 1),
+]
+
+
+@pytest.mark.parametrize("case", DGRAD_EPILOGUE, ids=[c[0] for c in DGRAD_EPILOGUE])
+def test_conv_data_gradient_epilogue(case):
+    """One data-gradient launch with every epilogue operand, as cb_step uses
+    it: accumulate, residual add (same shape or the option-A subsample),
+    ReLU mask, and the fused batch-norm backward partial sums, against the
+    oracle's data gradient with the epilogue applied by plain numpy."""
+    name, k, b, Ci, H, Co, R, st, pad, acc, use_mask, add_mode, add_C, bn, use_y = case
+    Ho = (H + 2 * pad - R) // st + 1
+    rng = _rng("dgrad" + name)
+    N = k * b
+    nw = Co * Ci * R * R
+    pstride = nw + 5
+    params = np.zeros(k * pstride, dtype=np.float32)
+    for j in range(k):
+        params[j * pstride:j * pstride + nw] = rng.standard_normal(nw) * np.sqrt(2.0 / (Ci * R * R))
+    dy = rng.standard_normal((N, Co, Ho, Ho), dtype=np.float32)
+    dx0 = rng.standard_normal((N, Ci, H, H), dtype=np.float32)
+    mask = rng.standard_normal((N, Ci, H, H), dtype=np.float32) if use_mask else None
+    add = None
+    if add_mode == 1:
+        add = rng.standard_normal((N, Ci, H, H), dtype=np.float32)
+    elif add_mode == 2:
+        add = rng.standard_normal((N, add_C, Ho, Ho), dtype=np.float32)
+    bn_x = rng.standard_normal((N, Ci, H, H), dtype=np.float32) if bn else None
+    bn_y = rng.standard_normal((N, Ci, H, H), dtype=np.float32) if (bn and use_y) else None
+    mean = (rng.standard_normal((k, Ci)) * 0.1).astype(np.float32) if bn else None
+    istd = (rng.uniform(0.5, 2.0, (k, Ci))).astype(np.float32) if bn else None
+    L = cb.lib()
+    parts = L.cb_test_conv_dgrad_parts(k, b, Ci, H, H, Co, R, st, pad)
+    assert parts > 0
+    d = {n_: (_dev(v) if v is not None else None) for n_, v in
+         dict(dy=dy, p=params, dx=dx0, mask=mask, add=add, x=bn_x, y=bn_y, mean=mean,
+              istd=istd).items()}
+    part = torch.zeros(k * Ci * parts * 2, dtype=torch.float64, device="cuda") if bn else None
+    ptr = lambda t: t.data_ptr() if t is not None else None
+    rc = L.cb_test_conv_dgrad(k, b, Ci, H, H, Co, R, st, pad, ptr(d["dy"]), ptr(d["p"]), pstride,
+                              ptr(d["dx"]), acc, ptr(d["mask"]), ptr(d["add"]), add_mode, add_C,
+                              ptr(d["x"]), ptr(d["y"]), ptr(d["mean"]), ptr(d["istd"]),
+                              ptr(part), torch.cuda.current_stream().cuda_stream)
+    assert rc == 0
+    torch.cuda.synchronize()
+    got = d["dx"].cpu().numpy()
+    sums = part.cpu().numpy().reshape(k, Ci, parts, 2).sum(axis=2) if bn else None
+    for j in sorted({0, k - 1}):
+        sl = slice(j * b, (j + 1) * b)
+        w = params[j * pstride:j * pstride + nw].reshape(Co, Ci, R, R)
+        _, ref, _, _ = oracle.conv2d(np.zeros((b, Ci, H, H), np.float32), w, None, st, pad,
+                                     dy=dy[sl])
+        if acc:
+            ref = ref + dx0[sl]
+        if add_mode == 1:
+            ref = ref + add[sl]
+        elif add_mode == 2:
+            ref[:, :, ::st, ::st] += add[sl][:, :Ci]
+        if use_mask:
+            ref = np.where(mask[sl] > 0, ref, 0.0)
+        assert max_rel(got[sl], ref) <= TOL_STEP1, (name, j, "dx")
+        if bn:
+            dd = ref if bn_y is None else np.where(bn_y[sl] > 0, ref, 0.0)
+            xh = (bn_x[sl].astype(np.float64) - mean[j][None, :, None, None]) * \
+                istd[j][None, :, None, None]
+            s1 = dd.sum(axis=(0, 2, 3))
+            s2 = (dd * xh).sum(axis=(0, 2, 3))
+            assert max_rel(sums[j, :, 0], s1) <= TOL_STEP1, (name, j, "sum d")
+            assert max_rel(sums[j, :, 1], s2) <= TOL_STEP1, (name, j, "sum d*xh")

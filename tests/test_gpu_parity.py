@@ -86,6 +86,31 @@ class Pair:
             err, where = per_tensor_max_rel(self.gpu.cb_get_grad(j), self.ref.grad(j), self.layout)
             assert err <= t, ("grad", j, err, where, "margin", m)
 
+    def check_grads_at_gpu_replicas(self):
+        """Each learner's gradient against the oracle's at the GPU's own
+        replica (after several steps the two trajectories differ by rounding,
+        and a ReLU decision within that distance of zero may go either way).
+        Where the oracle certifies every decision there: per tensor, strict.
+        Otherwise one flipped decision concentrates in one or two tensors
+        (up to 0.11 per tensor at 3 images of 16 x 16, measured on the oracle
+        itself), so the whole gradient vector's relative L2 takes the
+        ambiguity bound; the loss is strict either way."""
+        x, y = self.last
+        b = self.b
+        for j in range(self.k):
+            w = self.gpu.cb_get_replica(j)
+            xj, yj = x[j * b:(j + 1) * b], y[j * b:(j + 1) * b]
+            lj, gj = oracle.learner_grad(self.om, w, xj, yj)
+            m = oracle.learner_margin(self.om, w, xj, yj)
+            assert abs(self.gpu.cb_get_loss()[j] - lj) / abs(lj) <= TOL_STEP1
+            g = self.gpu.cb_get_grad(j)
+            if m >= MARGIN:
+                err, where = per_tensor_max_rel(g, gj, self.layout)
+                assert err <= TOL_STEP1, ("grad", j, err, where, "margin", m)
+            else:
+                err = rel_l2(g, gj)
+                assert err <= TOL_AMBIGUOUS, ("grad rel L2", j, err, "margin", m)
+
     def check_state(self, tol=TOL_STEP1):
         for j in range(self.k):
             err, where = per_tensor_max_rel(self.gpu.cb_get_replica(j), self.ref.replica(j),
@@ -275,9 +300,19 @@ def test_resnet32_ragged_batch():
     p.check_state()
     for t in range(1, 3):
         p.step(t)
-        p.check_grads(require_margin=False)
+        p.check_grads_at_gpu_replicas()
         p.sync()
     assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
+
+
+def test_resnet32_odd_feature_maps():
+    """28 x 28 images: stage 3 runs on 7 x 7 maps (the implicit-GEMM paths
+    with odd sizes, a global average over 49 pixels)."""
+    p = Pair("resnet32", 3, 28, 28, 10, k=2, b=3, seed=2)
+    p.step(0)
+    p.check_grads_at_gpu_replicas()
+    p.sync()
+    p.check_state(tol=TOL_AMBIGUOUS)
 
 
 def test_resnet32_k4_b32_full_size_learners():
