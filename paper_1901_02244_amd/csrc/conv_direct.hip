@@ -42,6 +42,18 @@ __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
 }
 __device__ __forceinline__ double shfl_xor_d(double v, int o) { return __shfl_xor(v, o, 64); }
 
+// Raw buffer reads: a wave-uniform descriptor over `bytes` bytes from base
+// and a 32-bit byte offset per lane.  An offset at or past `bytes` reads 0
+// (the buffer range check), which gives the tiles their zero border with
+// no branch: such lanes use OUTSIDE.
+constexpr uint32_t OUTSIDE = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t off_bytes) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off_bytes, 0, 0));
+}
+
 // Channel stride of the LDS input tile, rounded so that the four lane groups
 // of a wave fall in distinct 16-bank ranges.
 constexpr int pad_cs(int n) { return ((n + 47) / 64) * 64 + 16; }
@@ -120,34 +132,29 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
 
   float rx[NXT], rw[NWT];
   auto load = [&](const Tile& d, int c0) {
-    const float* IN = a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HW;
-    const float* Wt = a.w + (int64_t)d.j * a.pstride;
+    const auto src = buf_rsrc(a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HW,
+                              (uint32_t)(a.Cin * HW * 4));
+    const auto wsrc = buf_rsrc(a.w + (int64_t)d.j * a.pstride, (uint32_t)(a.Cin * a.Cout * 36));
 #pragma unroll
     for (int u = 0; u < NXT; ++u) {
       const int e = tid + u * 256;
-      float v = 0.f;
-      if (e < NX) {
-        const int ci = e / (HR * WP), rem = e - ci * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
-        const int ih = d.oh0 - 1 + hr, iw = wc - 1;
-        if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)WW)
-          v = IN[(int64_t)(c0 + ci) * HW + ih * WW + iw];
-      }
-      rx[u] = v;
+      const int ci = e / (HR * WP), rem = e - ci * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
+      const int ih = d.oh0 - 1 + hr, iw = wc - 1;
+      const bool ok = (NX % 256 == 0 || e < NX) && (unsigned)ih < (unsigned)H &&
+                      (unsigned)iw < (unsigned)WW;
+      rx[u] = buf_ld(src, ok ? (uint32_t)(((c0 + ci) * HW + ih * WW + iw) * 4) : OUTSIDE);
     }
 #pragma unroll
     for (int u = 0; u < NWT; ++u) {
       // e runs in memory order of the filter slice: row (co, or ci when
       // flipped), then a contiguous run within the row
       const int e = tid + u * 256;
-      float v = 0.f;
-      if (e < NW) {
-        const int row = e / WRUN, rem = e - row * WRUN;
-        if (!FLIP)  // filter [out = co0+row][in = c0 .. c0+CC)[tap]
-          v = Wt[((int64_t)(d.co0 + row) * a.Cin + c0) * 9 + rem];
-        else        // filter [its out = c0+row][its in = co0 .. co0+BN)[tap]
-          v = Wt[((int64_t)(c0 + row) * a.Cout + d.co0) * 9 + rem];
-      }
-      rw[u] = v;
+      const int row = e / WRUN, rem = e - row * WRUN;
+      // forward: filter [out = co0+row][in = c0 .. c0+CC)[tap]; flipped:
+      // filter [its out = c0+row][its in = co0 .. co0+BN)[tap]
+      const int el = FLIP ? ((c0 + row) * a.Cout + d.co0) * 9 + rem
+                          : ((d.co0 + row) * a.Cin + c0) * 9 + rem;
+      rw[u] = buf_ld(wsrc, (NW % 256 == 0 || e < NW) ? (uint32_t)(el * 4) : OUTSIDE);
     }
   };
   auto store = [&](int buf) {
@@ -421,30 +428,25 @@ __global__ __launch_bounds__(256) void conv3x3s2_dgrad_k(DirectArgs a) {
 
   float rx[NXT], rw[NWT];
   auto load = [&](const Tile& d, int c0) {
-    const float* DY = a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HWo;
-    const float* Wt = a.w + (int64_t)d.j * a.pstride;
+    const auto src = buf_rsrc(a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HWo,
+                              (uint32_t)(a.Cin * HWo * 4));
+    const auto wsrc = buf_rsrc(a.w + (int64_t)d.j * a.pstride, (uint32_t)(a.Cin * a.Cout * 36));
 #pragma unroll
     for (int u = 0; u < NXT; ++u) {
       const int e = tid + u * 256;
-      float v = 0.f;
-      if (e < NX) {
-        const int c = e / (HRo * WPo), rem = e - c * (HRo * WPo), hr = rem / WPo, wc = rem - hr * WPo;
-        const int m = d.m0 + hr;
-        if (m < HO && wc < WO) v = DY[(int64_t)(c0 + c) * HWo + m * WO + wc];
-      }
-      rx[u] = v;
+      const int c = e / (HRo * WPo), rem = e - c * (HRo * WPo), hr = rem / WPo, wc = rem - hr * WPo;
+      const int m = d.m0 + hr;
+      const bool ok = (NX % 256 == 0 || e < NX) && m < HO && wc < WO;
+      rx[u] = buf_ld(src, ok ? (uint32_t)(((c0 + c) * HWo + m * WO + wc) * 4) : OUTSIDE);
     }
 #pragma unroll
     for (int u = 0; u < NWT; ++u) {
       // the filter [co][ci][tap] of the convolution: rows co = c0 + row (the
       // contraction), runs over ci in the tile and the taps
       const int e = tid + u * 256;
-      float v = 0.f;
-      if (e < NW) {
-        const int row = e / WRUN, rem = e - row * WRUN;
-        v = Wt[((int64_t)(c0 + row) * a.Cout + d.co0) * 9 + rem];
-      }
-      rw[u] = v;
+      const int row = e / WRUN, rem = e - row * WRUN;
+      const int el = ((c0 + row) * a.Cout + d.co0) * 9 + rem;
+      rw[u] = buf_ld(wsrc, (NW % 256 == 0 || e < NW) ? (uint32_t)(el * 4) : OUTSIDE);
     }
   };
   auto store = [&](int buf) {
@@ -709,17 +711,15 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
         ra[i] = *reinterpret_cast<const v4f*>(DY + (int64_t)c * HW + q * 4);
       }
     }
+    const auto xsrc = buf_rsrc(X, (uint32_t)(16 * HW * 4));
 #pragma unroll
     for (int i = 0; i < NXT; ++i) {
       const int e = tid + i * 256;
-      float v = 0.f;
-      if (e < NX) {
-        const int c = e / (HR * WP), rem = e - c * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
-        const int ih = h0 - 1 + hr, iw = wc - 1;
-        if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)WW)
-          v = X[(int64_t)c * HW + ih * WW + iw];
-      }
-      rx[i] = v;
+      const int c = e / (HR * WP), rem = e - c * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
+      const int ih = h0 - 1 + hr, iw = wc - 1;
+      const bool ok = (NX % 256 == 0 || e < NX) && (unsigned)ih < (unsigned)H &&
+                      (unsigned)iw < (unsigned)WW;
+      rx[i] = buf_ld(xsrc, ok ? (uint32_t)((c * HW + ih * WW + iw) * 4) : OUTSIDE);
     }
     __syncthreads();  // the previous unit's reads of the tiles are done
 #pragma unroll
