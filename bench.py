@@ -386,6 +386,13 @@ def main():
     log(f"[bench] {wk.name}: {ms:.3f} ms/step (wall {wall:.3f}), {value:.0f} images/s")
     roof = roofline_of(prof)
     tot = sum(v[1] for v in prof.values())
+    # the whole step against the fp32 MFMA peak: every contraction's
+    # algorithmic FLOPs of one step over the timed (uninstrumented) step time
+    step_flops = sum(v[2] for v in prof.values())
+    step_util = {"flop_per_step": round(step_flops), "flop_per_image": round(step_flops / wk.n_images),
+                 "TFLOP/s": round(step_flops / (ms * 1e-3) / 1e12, 2),
+                 "mfma_frac": round(step_flops / (ms * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFS, 4)}
+    log(f"[bench] whole step: {step_util}")
     def kernel_entry(v):
         e = {"launches_per_step": v[0], "ms_per_step": round(v[1], 4), "share": round(v[1] / tot, 4),
              "GB/s": round(v[3] / (v[1] * 1e-3) / 1e9, 1)}
@@ -442,6 +449,7 @@ def main():
                                "one SMA iteration per step",
                    "k": wk.k, "b": wk.b, "images_per_step": wk.n_images},
         "roofline": roof,
+        "step_mfma_utilisation": step_util,
         "kernels_per_step": kernels,
         "k_sweep_b16": sweep,
         "k_sweep_best": max(sweep, key=lambda k: sweep[k]["images_per_s"]) if sweep else None,

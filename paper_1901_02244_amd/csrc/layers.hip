@@ -196,26 +196,36 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 constexpr int BN_U = 4;
 
 struct Quad {
-  int64_t off;  // element offset of the quad from the (replica, channel) base
-  int p;        // pixel of its first element
-  int img;      // image within the replica
+  int off;   // element offset of the quad from the (replica, channel) base
+  int p;     // pixel of its first element
+  int img;   // image within the replica
   bool ok;
 };
 
-__device__ __forceinline__ Quad quad_at(int q, int q1, int HW4, int CHW) {
+// Quad q of a (replica, channel): image q / HW4, pixel 4 (q % HW4).  Planes
+// whose quad count is a power of two (sh >= 0) divide by shifting.
+__device__ __forceinline__ Quad quad_at(int q, int q1, int HW4, int sh, int CHW) {
   Quad r;
   r.ok = q < q1;
   const int qq = r.ok ? q : 0;
-  r.img = qq / HW4;
-  r.p = (qq - r.img * HW4) * 4;
-  r.off = (int64_t)r.img * CHW + r.p;
+  if (sh >= 0) {
+    r.img = qq >> sh;
+    r.p = (qq & (HW4 - 1)) * 4;
+  } else {
+    r.img = qq / HW4;
+    r.p = (qq - r.img * HW4) * 4;
+  }
+  r.off = r.img * CHW + r.p;
   return r;
 }
+
+__device__ __forceinline__ int pow2_shift(int n) { return (n & (n - 1)) == 0 ? __builtin_ctz(n) : -1; }
 
 __global__ __launch_bounds__(256) void bn_apply_v4_k(BNArgs a) {
   __shared__ double red[8];
   const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
   const int HW = a.H * a.W, HW4 = HW >> 2, n4 = a.b * HW4, CHW = a.C * HW;
+  const int sh = pow2_shift(HW4);
   const int per = (n4 + a.chunks - 1) / a.chunks;
   const int q0 = chunk * per, q1 = min(n4, q0 + per);
   const int64_t base = ((int64_t)j * a.b * a.C + c) * HW;
@@ -227,7 +237,7 @@ __global__ __launch_bounds__(256) void bn_apply_v4_k(BNArgs a) {
   auto load = [&]() {
 #pragma unroll
     for (int u = 0; u < BN_U; ++u) {
-      qd[u] = quad_at(qb + u * 256, q1, HW4, CHW);
+      qd[u] = quad_at(qb + u * 256, q1, HW4, sh, CHW);
       if (qd[u].ok) {
         xv[u] = *reinterpret_cast<const v4f*>(X + qd[u].off);
         if (a.res_mode == RES_SAME) rv[u] = *reinterpret_cast<const v4f*>(a.res + base + qd[u].off);
@@ -285,6 +295,7 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_v4_k(BNBwdArgs a) {
   __shared__ double red[8];
   const int chunk = blockIdx.x, c = blockIdx.y, j = blockIdx.z;
   const int HW = a.H * a.W, HW4 = HW >> 2, n4 = a.b * HW4, CHW = a.C * HW;
+  const int sh = pow2_shift(HW4);
   const int per = (n4 + a.chunks - 1) / a.chunks;
   const int q0 = chunk * per, q1 = min(n4, q0 + per);
   const int64_t base = ((int64_t)j * a.b * a.C + c) * HW;
@@ -294,7 +305,7 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_v4_k(BNBwdArgs a) {
   auto load = [&]() {
 #pragma unroll
     for (int u = 0; u < BN_U; ++u) {
-      qd[u] = quad_at(qb + u * 256, q1, HW4, CHW);
+      qd[u] = quad_at(qb + u * 256, q1, HW4, sh, CHW);
       if (qd[u].ok) {
         const int64_t o = base + qd[u].off;
         dv[u] = *reinterpret_cast<const v4f*>(a.dy + o);
