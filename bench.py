@@ -253,6 +253,17 @@ def lenet_latency(iters=200):
             "images_per_s": round(wk.n_images / ms * 1e3, 1)}
 
 
+def resnet50_throughput(steps=5, warmup=2):
+    """ResNet-50, k = 2 learners of 32 images at 224 x 224: images/s."""
+    import workloads as wl
+
+    wk = wl.RESNET50_K2
+    ms, _, _ = time_training(wk, steps, warmup, ring=2)
+    log(f"[bench] ResNet-50 k=2 b=32: {ms:.2f} ms/iteration, {wk.n_images / ms * 1e3:.0f} images/s")
+    return {"ms_per_iteration": round(ms, 3), "images_per_s": round(wk.n_images / ms * 1e3, 1),
+            "steps": steps}
+
+
 def sma_micro(steps=20, warmup=3):
     """Fused SMA kernel alone on ResNet-50's P with k = 32 replicas."""
     import torch
@@ -422,6 +433,7 @@ def main():
         extra["ssgd_baseline_same_kernels"] = ssgd_baseline(wk)
         extra["autotune_alg2_b16"] = autotune(wl.RESNET32_SWEEP)
         extra["lenet_k8_b16"] = lenet_latency()
+        extra["resnet50_k2_b32"] = resnet50_throughput()
     micro = None
     if not args.no_micro:
         micro = sma_micro()

@@ -367,6 +367,39 @@ def test_resnet32_k4_b32_hundred_iterations():
     assert err <= max(TOL_Z_L2, 2 * env["100"]), (err, env["100"])
 
 
+def test_resnet32_k32_b16_full_size_learners():
+    """The largest point of the k sweep: 32 ResNet-32 learners of 16 images
+    in every launch (other tile choices and grids than at k = 4).  The
+    oracle recomputes learners 0, 17 and 31; losses strict, gradients with
+    the margin rule; then one synchronisation against the SMA kernel's
+    oracle on the GPU's own gradients."""
+    k, b = 32, 16
+    wk = wl.RESNET32_SWEEP.with_k(k)
+    m = cb.model("resnet32", 3, 32, 32, 10)
+    layout = cb.cb_tensor_layout(m)
+    w0 = wl.init_w0(layout, wk.seed)
+    ctx = cb.Context(m, k, b, 1.0 / k, wk.lr, wk.momentum, w0)
+    x, y = wl.workload_batch(wk, 0)
+    ctx.cb_step(_dev(x), _dev(y))
+    loss = ctx.cb_get_loss()
+    om = oracle.model("resnet32", 3, 32, 32, 10)
+    for j in (0, 17, 31):
+        xj, yj = x[j * b:(j + 1) * b], y[j * b:(j + 1) * b]
+        lj, gj = oracle.learner_grad(om, w0, xj, yj)
+        assert abs(loss[j] - lj) / abs(lj) <= TOL_STEP1
+        margin = oracle.learner_margin(om, w0, xj, yj)
+        tol = TOL_STEP1 if margin >= MARGIN else TOL_AMBIGUOUS
+        err, where = per_tensor_max_rel(ctx.cb_get_grad(j), gj, layout)
+        assert err <= tol, (j, err, where, "margin", margin)
+    G = np.stack([ctx.cb_get_grad(j) for j in range(k)])
+    ctx.cb_sync()
+    W = np.tile(w0, (k, 1))
+    Wn, _, Zn, _ = oracle.sma_update(W, G, w0, w0, f32(1.0 / k), f32(wk.lr), f32(wk.momentum))
+    assert max_rel(ctx.cb_get_central(), Zn) <= 1e-6
+    for j in (0, 31):
+        assert max_rel(ctx.cb_get_replica(j), Wn[j]) <= 1e-6
+
+
 def test_resnet50_k2_b32_full_size_learner0():
     """Full-size ResNet-50 workload (k = 2 learners of 32 images, 224x224):
     learner 0's loss and sampled gradient entries against the oracle's
