@@ -629,7 +629,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
       case OP_XENT: break;
       case OP_GAP:
         CB_LAUNCH(c, "gap_bwd_k", 0.0, 4.0 * N * o.C * (o.H * o.W + 1.0),
-                  gap_bwd(grd(o.out), N, o.C, o.H * o.W, grd(o.in), s));
+                  gap_bwd(grd(o.out), N, o.C, o.H * o.W, grd(o.in), s, &nm_));
         break;
       case OP_MAXPOOL:
         CB_LAUNCH(c, "maxpool_bwd_k", 0.0,

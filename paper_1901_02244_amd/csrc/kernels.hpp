@@ -207,7 +207,8 @@ hipError_t maxpool_bwd(const float* dy, const int* arg, const float* x, int N, i
                        int W, int K, int st, int pad, int Ho, int Wo, float* dx, int mask_relu,
                        hipStream_t s);
 hipError_t gap_fwd(const float* x, int N, int C, int HW, float* y, hipStream_t s);
-hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t s);
+hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t s,
+                   const char** name = nullptr);
 // Mean softmax cross-entropy per replica and its gradient wrt the logits.
 hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b, int classes,
                         float* dlogits, float* loss, hipStream_t s);

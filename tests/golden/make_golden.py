@@ -9,6 +9,7 @@ Run from the repository root:
     python tests/golden/make_golden.py resnet32_z10      # ~4 min
     python tests/golden/make_golden.py resnet32_envelope # ~1 h
     python tests/golden/make_golden.py resnet50_sampled  # ~10 min
+    python tests/golden/make_golden.py lenet_z1000       # ~5 min
 
 Jobs:
   lenet_envelope / resnet32_envelope: how far the oracle drifts from itself
@@ -20,6 +21,9 @@ Jobs:
     iterations of ResNet-32, k = 4 learners of batch 32 (float32 .npy).
   resnet50_sampled: learner 0's loss and sampled gradient entries after one
     forward/backward pass of ResNet-50 on 224x224 images, b = 32.
+  lenet_z1000: LeNet-5, k = 8 learners of 16, the full 1000 SMA iterations:
+    the central model after 1000 (float32 .npy) and the oracle's drift
+    from itself (as in the envelope jobs) after 100, 300 and 1000.
 """
 import json
 import os
@@ -53,7 +57,8 @@ def run_sma(wk, steps, w0, keep=()):
         assert s.sync() == 0
         if t + 1 in keep:
             kept[t + 1] = s.central()
-        print(f"{wk.name} step {t + 1}", flush=True)
+        if (t + 1) % 10 == 0 or t + 1 == steps:
+            print(f"{wk.name} step {t + 1}", flush=True)
     return s, kept
 
 
@@ -113,6 +118,23 @@ def resnet50_sampled(per_tensor=24):
               open(os.path.join(HERE, "resnet50_k2_b32_learner0.json"), "w"))
 
 
+def lenet_z1000():
+    wk = wl.LENET_K8
+    keep = (100, 300, 1000)
+    t0 = time.time()
+    s, a = run_sma(wk, 1000, w0_of(wk), keep=keep)
+    _, b = run_sma(wk, 1000, w0_of(wk, PERTURB), keep=keep)
+    np.save(os.path.join(HERE, "lenet5_k8_b16_z1000.npy"), a[1000].astype(np.float32))
+    env = {str(t): float(np.linalg.norm(a[t] - b[t]) / np.linalg.norm(a[t])) for t in keep}
+    json.dump({"workload": wk.name, "steps": 1000, "file": "lenet5_k8_b16_z1000.npy",
+               "dtype": "float32 (oracle fp64 rounded)", "seconds": round(time.time() - t0),
+               "perturbation": PERTURB,
+               "what": "relative L2 distance between the oracle's central models from w0 and from "
+                       "w0*(1+1e-7*N(0,1)) after each listed number of SMA iterations",
+               "rel_l2": env},
+              open(os.path.join(HERE, "lenet5_k8_b16_z1000.json"), "w"), indent=1)
+
+
 if __name__ == "__main__":
     job = sys.argv[1]
     if job == "lenet_envelope":
@@ -123,6 +145,8 @@ if __name__ == "__main__":
         resnet32_z(100)
     elif job == "resnet32_z10":
         resnet32_z(10)
+    elif job == "lenet_z1000":
+        lenet_z1000()
     elif job == "resnet50_sampled":
         resnet50_sampled()
     else:

@@ -174,6 +174,46 @@ def test_sma_microbench_size_sampled():
         assert max_rel(ctx.cb_get_replica(j)[idx], Wn[j]) <= 1e-6
 
 
+def test_sma_kernel_invariants():
+    """The method's invariants on the GPU kernel itself:
+    identical replicas at zero velocity with zero gradient leave everything
+    (z, z_prev, the replicas) bitwise unchanged; and the corrections added
+    to z equal those removed from the replicas:
+    sum_j (w_j - lr g_j - w_j') = z' - z - mu (z - z_prev)."""
+    k, lr, mu = 5, 0.05, 0.9
+    m = cb.model("resnet32", *MODEL_SHAPES["resnet32"])
+    P = cb.cb_num_params(m)
+    W, G, Z, Zp = wl.random_state(k, P, seed=21)
+    ctx = cb.Context(m, k, 1, 0.3, lr, mu, Z)
+    # fixed point
+    ctx.cb_set_state(np.tile(Z, (k, 1)), Z, Z)
+    ctx.cb_sma_apply(_dev(np.zeros((k, P), np.float32)))
+    np.testing.assert_array_equal(ctx.cb_get_central(), Z)
+    np.testing.assert_array_equal(ctx.cb_get_prev_central(), Z)
+    for j in (0, k - 1):
+        np.testing.assert_array_equal(ctx.cb_get_replica(j), Z)
+    # conservation of the corrections, at fp32 resolution
+    ctx.cb_set_state(W, Z, Zp)
+    ctx.cb_sma_apply(_dev(G))
+    Wn = np.stack([ctx.cb_get_replica(j) for j in range(k)]).astype(np.float64)
+    removed = (W.astype(np.float64) - lr * G.astype(np.float64) - Wn).sum(axis=0)
+    added = ctx.cb_get_central().astype(np.float64) - Z - mu * (Z.astype(np.float64) - Zp)
+    scale = np.abs(W).max() * k
+    assert np.abs(removed - added).max() <= 1e-6 * scale
+
+
+def test_one_learner_no_correction_is_momentum_sgd():
+    """k = 1, alpha = 0 with learner momentum mu is heavy-ball SGD (Eq. 3):
+    the replica follows the oracle, and z never moves from w0 (bitwise)."""
+    p = Pair("lenet5", 1, 28, 28, 10, k=1, b=8, alpha=0.0, mu_l=0.9, seed=5)
+    for t in range(4):
+        p.step(t)
+        p.sync()
+    np.testing.assert_array_equal(p.gpu.cb_get_central(), p.w0)
+    p.check_state(tol=TOL_AMBIGUOUS)
+    assert rel_l2(p.gpu.cb_get_replica(0), p.ref.replica(0)) <= TOL_Z_L2
+
+
 # ------------------------------------------------------------- end to end
 
 def test_lenet_k2_b4_ten_iterations():
@@ -207,6 +247,26 @@ def test_lenet_k8_b16_hundred_iterations():
             assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
     err = rel_l2(p.gpu.cb_get_central(), p.ref.central())
     assert err <= max(TOL_Z_L2, 2 * env["100"]), (err, env["100"])
+
+
+def test_lenet_k8_b16_thousand_iterations():
+    """The LeNet workload as specified: k = 8 learners of 16, 1000 SMA
+    iterations with a synchronisation every iteration, against the oracle's
+    stored central model (tests/golden/make_golden.py lenet_z1000).  The
+    oracle drifts from itself by the stored amount when w0 moves by one part
+    in 1e7, so the bound is the larger of 1e-3 and twice that drift."""
+    meta = json.load(open(os.path.join(GOLDEN, "lenet5_k8_b16_z1000.json")))
+    z1000 = np.load(os.path.join(GOLDEN, meta["file"]))
+    wk = wl.LENET_K8
+    m = cb.model("lenet5", wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
+    ctx = cb.Context(m, wk.k, wk.b, wk.alpha, wk.lr, wk.momentum,
+                     wl.init_w0(cb.cb_tensor_layout(m), wk.seed))
+    for t in range(1000):
+        x, y = wl.workload_batch(wk, t)
+        ctx.cb_step(_dev(x), _dev(y))
+        ctx.cb_sync()
+    err = rel_l2(ctx.cb_get_central(), z1000)
+    assert err <= max(TOL_Z_L2, 2 * meta["rel_l2"]["1000"]), (err, meta["rel_l2"])
 
 
 def test_lenet_learner_momentum_and_unsynced_steps():
