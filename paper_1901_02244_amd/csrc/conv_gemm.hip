@@ -572,6 +572,50 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Fully connected layers (a 1x1 convolution on 1x1 images) with few inputs
+// per output: the tile machinery of the implicit GEMM costs more than the
+// arithmetic there.
+// Forward: one wave per output y[n][co] = sum_ci x[n][ci] w[co][ci] (+ b),
+// lanes over ci, a fixed-order wave sum.
+__global__ __launch_bounds__(256) void fc_fwd_k(const float* x, const float* w, const float* bias,
+                                                int64_t pstride, int b, int Ci, int Co, int relu,
+                                                float* y) {
+  const int lane = threadIdx.x & 63;
+  const int64_t o = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // over k*b*Co outputs
+  const int j = blockIdx.y;
+  if (o >= (int64_t)b * Co) return;
+  const int n = (int)(o / Co), co = (int)(o - (int64_t)n * Co);
+  const float* X = x + ((int64_t)j * b + n) * Ci;
+  const float* Wr = w + (int64_t)j * pstride + (int64_t)co * Ci;
+  float s = 0.f;
+  for (int ci = lane; ci < Ci; ci += 64) s += X[ci] * Wr[ci];
+  s = wave_sum(s);
+  if (lane == 0) {
+    if (bias) s += bias[(int64_t)j * pstride + co];
+    if (relu) s = s > 0.f ? s : 0.f;
+    y[((int64_t)j * b + n) * Co + co] = s;
+  }
+}
+
+// Data gradient: one thread per dX[n][ci] = sum_co dY[n][co] w[co][ci], in
+// co order; then accumulate and the ReLU mask as in the GEMM epilogue.
+__global__ __launch_bounds__(256) void fc_dgrad_k(const float* dy, const float* w, int64_t pstride,
+                                                  int b, int Ci, int Co, int accumulate,
+                                                  const float* mask, float* dx) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;  // over b*Ci of replica j
+  const int j = blockIdx.y;
+  if (i >= (int64_t)b * Ci) return;
+  const int n = (int)(i / Ci), ci = (int)(i - (int64_t)n * Ci);
+  const float* D = dy + ((int64_t)j * b + n) * Co;
+  const float* Wt = w + (int64_t)j * pstride + ci;
+  float s = 0.f;
+  for (int co = 0; co < Co; ++co) s += D[co] * Wt[(int64_t)co * Ci];
+  const int64_t g = ((int64_t)j * b + n) * Ci + ci;
+  if (accumulate) s += dx[g];
+  if (mask && !(mask[g] > 0.f)) s = 0.f;
+  dx[g] = s;
+}
+
 // db[j][c]: one block per (c, j), fixed-order reduction.
 __global__ __launch_bounds__(256) void channel_sum_k(const float* dy, int b, int C, int HW,
                                                      float* db, int64_t pstride) {
@@ -731,7 +775,23 @@ bool conv_supported(int R, int S, int st, bool need_dx) {
   return false;
 }
 
+// The FC kernels take layers with at most FC_MAX_K inputs per output
+// (forward) or FC_MAX_DK outputs per input (data gradient), without fused
+// BN partials.
+constexpr int FC_MAX_K = 1024, FC_MAX_DK = 256;
+
+bool fc_layer(const ConvGeom& g) {
+  return g.R == 1 && g.S == 1 && g.H == 1 && g.W == 1 && g.st == 1 && g.pad == 0;
+}
+
 hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
+  if (fc_layer(a.g) && !a.stats && a.g.Ci <= FC_MAX_K) {
+    const int64_t outs = (int64_t)a.g.b * a.g.Co;
+    klaunch(fc_fwd_k, dim3(cdiv(outs, 4), a.g.k), dim3(256), 0, s, a.x, a.w, a.bias, a.pstride,
+            a.g.b, a.g.Ci, a.g.Co, a.relu, a.y);
+    if (name) *name = "fc_fwd_k";
+    return hipGetLastError();
+  }
   // the direct kernel moves its outputs in 16-byte pieces (workspace
   // tensors are 256-byte aligned, so layers of a plan always qualify)
   if (conv_direct_fwd_ok(a.g) && al16(a.y)) return conv_direct_fwd(a, s, name);
@@ -745,6 +805,12 @@ hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
 }
 
 hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
+  if (fc_layer(a.g) && !a.bn_part && a.add_mode == ADD_NONE && a.g.Co <= FC_MAX_DK) {
+    klaunch(fc_dgrad_k, dim3(cdiv((int64_t)a.g.b * a.g.Ci, 256), a.g.k), dim3(256), 0, s, a.dy,
+            a.w, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.accumulate, a.mask, a.dx);
+    if (name) *name = "fc_dgrad_k";
+    return hipGetLastError();
+  }
   const bool vec_ok = al16(a.dx) && al16(a.mask) && al16(a.bn_x) && al16(a.bn_y) && al16(a.add);
   if (conv_direct_bwd_data_ok(a.g) && vec_ok) return conv_direct_bwd_data(a, s, name);
   if (conv_s2_dgrad_ok(a.g) && vec_ok && (a.add_mode != ADD_SUBSAMPLE || a.add_st == 2))
