@@ -28,9 +28,6 @@
 #ifndef TAP_UNROLL
 #define TAP_UNROLL 9
 #endif
-#ifndef CG_UNROLL
-#define CG_UNROLL 4
-#endif
 
 namespace cbk {
 namespace {
@@ -84,25 +81,31 @@ struct DirectArgs {
 template <int WW, int TH, int BN, int CC, bool FLIP>
 __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   constexpr int WP = WW + 2, HR = TH + 2;
-  constexpr int CS = pad_cs(HR * WP);     // LDS channel stride of the input tile
+  constexpr int NPIX = HR * WP;           // pixels of the input tile (with border)
   constexpr int M = TH * WW;              // output pixels per tile
   constexpr int TM = M / 64;              // 16-pixel blocks per wave (waves split M)
   constexpr int TN = BN / 16;
-  // Filter tile in LDS, in the filter's own memory order so that stores
-  // are contiguous: forward [co][ci][tap] with row stride WS (146 = 144 + 2
-  // spreads the 16 columns x 4 channels of an operand read over the banks);
-  // data gradient [ci][co][8 - tap] (the flipped filter as stored) with row
-  // stride WS.
-  constexpr int WS = FLIP ? (BN == 16 ? 144 : 304) : CC * 9 + 2;
-  constexpr int WROWS = FLIP ? CC : BN;
-  constexpr int WRUN = FLIP ? BN * 9 : CC * 9;  // contiguous run of one row
-  constexpr int NX = CC * HR * WP;        // input-tile elements per chunk
+  constexpr int C4 = CC / 4;              // channel quads per chunk
+  // LDS tiles hold four consecutive channels of a pixel (or of a filter
+  // row and tap) as one 16-byte quad, so that one ds_read_b128 gives a lane
+  // the operands of four MFMAs.  Within an MFMA the lane group kq = lane / 16
+  // takes channel 16g + 4kq + q of the quad read for MFMA (g, q).
+  // Input tile: [pixel][CC channels], pixel stride PS = CC + 4 floats (the
+  // padding puts the 16 pixels of a read, and of a store, on distinct banks).
+  // Filter tile: [row][tap][CC channels], row stride WS = 9 CC + 4; a row
+  // is an output channel of the forward, an output channel of the data
+  // gradient (input channel of the filter) when flipped; the flipped
+  // filter's taps are read in reverse (8 - tap).
+  constexpr int PS = CC + 4;
+  constexpr int WS = 9 * CC + 4;
+  constexpr int NX = C4 * NPIX;           // input quads per chunk
   constexpr int NXT = (NX + 255) / 256;
-  constexpr int NW = 9 * CC * BN;         // filter elements per chunk
+  constexpr int NW = BN * 9 * C4;         // filter quads per chunk
   constexpr int NWT = (NW + 255) / 256;
   static_assert(TM >= 1 && M % 64 == 0, "tile must cover whole 64-pixel wave strips");
-  __shared__ __attribute__((aligned(16))) float xs[2][CC * CS];
-  __shared__ __attribute__((aligned(16))) float ws[2][WROWS * WS];
+  static_assert(CC % 16 == 0, "a chunk is whole 16-channel MFMA groups");
+  __shared__ __attribute__((aligned(16))) float xs[2][NPIX * PS];
+  __shared__ __attribute__((aligned(16))) float ws[2][BN * WS];
   __shared__ double red[4][BN][2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4;
@@ -130,63 +133,93 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
     return d;
   };
 
-  float rx[NXT], rw[NWT];
+  v4f rx[NXT], rw[NWT];
   auto load = [&](const Tile& d, int c0) {
     const auto src = buf_rsrc(a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HW,
                               (uint32_t)(a.Cin * HW * 4));
     const auto wsrc = buf_rsrc(a.w + (int64_t)d.j * a.pstride, (uint32_t)(a.Cin * a.Cout * 36));
 #pragma unroll
     for (int u = 0; u < NXT; ++u) {
+      // quad e: channels c0 + 4 c4 .. +3 of tile pixel pix; consecutive
+      // lanes take consecutive pixels, so each of the four reads is
+      // coalesced along the image row
       const int e = tid + u * 256;
-      const int ci = e / (HR * WP), rem = e - ci * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
+      const int c4 = e / NPIX, pix = e - c4 * NPIX, hr = pix / WP, wc = pix - hr * WP;
       const int ih = d.oh0 - 1 + hr, iw = wc - 1;
       const bool ok = (NX % 256 == 0 || e < NX) && (unsigned)ih < (unsigned)H &&
                       (unsigned)iw < (unsigned)WW;
-      rx[u] = buf_ld(src, ok ? (uint32_t)(((c0 + ci) * HW + ih * WW + iw) * 4) : OUTSIDE);
+      const uint32_t o = (uint32_t)(((c0 + 4 * c4) * HW + ih * WW + iw) * 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) rx[u][q] = buf_ld(src, ok ? o + (uint32_t)(q * HW * 4) : OUTSIDE);
     }
 #pragma unroll
     for (int u = 0; u < NWT; ++u) {
-      // e runs in memory order of the filter slice: row (co, or ci when
-      // flipped), then a contiguous run within the row
+      // quad e: row, tap, four consecutive channels of the chunk.  Forward:
+      // filter [co0 + row][c0 + 4 c4 + q][tap]; flipped: filter
+      // [c0 + 4 c4 + q][co0 + row][tap], enumerated with row and tap
+      // fastest so that the reads follow memory order.
       const int e = tid + u * 256;
-      const int row = e / WRUN, rem = e - row * WRUN;
-      // forward: filter [out = co0+row][in = c0 .. c0+CC)[tap]; flipped:
-      // filter [its out = c0+row][its in = co0 .. co0+BN)[tap]
-      const int el = FLIP ? ((c0 + row) * a.Cout + d.co0) * 9 + rem
-                          : ((d.co0 + row) * a.Cin + c0) * 9 + rem;
-      rw[u] = buf_ld(wsrc, (NW % 256 == 0 || e < NW) ? (uint32_t)(el * 4) : OUTSIDE);
+      int row, tap, c4;
+      if (FLIP) {
+        c4 = e / (BN * 9);
+        const int rem = e - c4 * (BN * 9);
+        row = rem / 9;
+        tap = rem - row * 9;
+      } else {
+        row = e / (9 * C4);
+        const int rem = e - row * (9 * C4);
+        tap = rem / C4;
+        c4 = rem - tap * C4;
+      }
+      const bool ok = NW % 256 == 0 || e < NW;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int el = FLIP ? ((c0 + 4 * c4 + q) * a.Cout + d.co0 + row) * 9 + tap
+                            : ((d.co0 + row) * a.Cin + c0 + 4 * c4 + q) * 9 + tap;
+        rw[u][q] = buf_ld(wsrc, ok ? (uint32_t)(el * 4) : OUTSIDE);
+      }
     }
   };
   auto store = [&](int buf) {
 #pragma unroll
     for (int u = 0; u < NXT; ++u) {
       const int e = tid + u * 256;
-      if (e < NX) {
-        const int ci = e / (HR * WP), rem = e - ci * (HR * WP);
-        xs[buf][ci * CS + rem] = rx[u];
+      if (NX % 256 == 0 || e < NX) {
+        const int c4 = e / NPIX, pix = e - c4 * NPIX;
+        *reinterpret_cast<v4f*>(&xs[buf][pix * PS + 4 * c4]) = rx[u];
       }
     }
 #pragma unroll
     for (int u = 0; u < NWT; ++u) {
       const int e = tid + u * 256;
-      if (e < NW) {
-        const int row = e / WRUN;
-        ws[buf][row * WS + (e - row * WRUN)] = rw[u];
+      if (NW % 256 == 0 || e < NW) {
+        int row, tap, c4;
+        if (FLIP) {
+          c4 = e / (BN * 9);
+          const int rem = e - c4 * (BN * 9);
+          row = rem / 9;
+          tap = rem - row * 9;
+        } else {
+          row = e / (9 * C4);
+          const int rem = e - row * (9 * C4);
+          tap = rem / C4;
+          c4 = rem - tap * C4;
+        }
+        *reinterpret_cast<v4f*>(&ws[buf][row * WS + tap * CC + 4 * c4]) = rw[u];
       }
     }
   };
 
-  // lane bases: pixel of each of this wave's 16-pixel blocks, and column
+  // lane bases: LDS quad of each of this wave's 16-pixel blocks (tap 0,
+  // channel group 0), and of the lane's filter row
   int xbase[TM];
 #pragma unroll
   for (int t = 0; t < TM; ++t) {
     const int m = (wave * TM + t) * 16 + (lane & 15);
     const int ohl = m / WW, ow = m - ohl * WW;
-    xbase[t] = kq * CS + ohl * WP + ow;
+    xbase[t] = (ohl * WP + ow) * PS + 4 * kq;
   }
-  // B operand of lane (kq, l16): input channel cg*4 + kq, output channel
-  // u*16 + l16 of the tile
-  const int wbase = FLIP ? kq * WS + (lane & 15) * 9 : (lane & 15) * WS + kq * 9;
+  const int wbase = (lane & 15) * WS + 4 * kq;
 
   // Epilogue operands of the data gradient (ReLU mask, the next batch
   // norm's x and y), loaded together with the inputs of the tile before, so
@@ -337,19 +370,22 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
 #pragma unroll TAP_UNROLL
       for (int tap = 0; tap < 9; ++tap) {
         const int r = tap / 3, s = tap - r * 3;
-#pragma unroll CG_UNROLL
-        for (int cg = 0; cg < CC / 4; ++cg) {
-          float av[TM], bv[TN];
+        const int tw = FLIP ? 8 - tap : tap;
 #pragma unroll
-          for (int x = 0; x < TM; ++x) av[x] = X[xbase[x] + cg * 4 * CS + r * WP + s];
-#pragma unroll
-          for (int u = 0; u < TN; ++u)
-            bv[u] = FLIP ? Wl[wbase + cg * 4 * WS + u * 144 + (8 - tap)]
-                         : Wl[wbase + u * 16 * WS + cg * 36 + tap];
+        for (int g = 0; g < CC / 16; ++g) {
+          v4f av[TM], bv[TN];
 #pragma unroll
           for (int x = 0; x < TM; ++x)
+            av[x] = *reinterpret_cast<const v4f*>(&X[xbase[x] + (r * WP + s) * PS + 16 * g]);
 #pragma unroll
-            for (int u = 0; u < TN; ++u) acc[x][u] = mfma4(av[x], bv[u], acc[x][u]);
+          for (int u = 0; u < TN; ++u)
+            bv[u] = *reinterpret_cast<const v4f*>(&Wl[wbase + u * 16 * WS + tw * CC + 16 * g]);
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int x = 0; x < TM; ++x)
+#pragma unroll
+              for (int u = 0; u < TN; ++u) acc[x][u] = mfma4(av[x][q], bv[u][q], acc[x][u]);
         }
       }
       if (has_next) store(cur ^ 1);
