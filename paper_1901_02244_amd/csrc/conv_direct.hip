@@ -104,8 +104,11 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   constexpr int NWT = (NW + 255) / 256;
   static_assert(TM >= 1 && M % 64 == 0, "tile must cover whole 64-pixel wave strips");
   static_assert(CC % 16 == 0, "a chunk is whole 16-channel MFMA groups");
-  __shared__ __attribute__((aligned(16))) float xs[2][NPIX * PS];
-  __shared__ __attribute__((aligned(16))) float ws[2][BN * WS];
+  // One LDS copy of each tile: the next chunk waits in registers until
+  // every wave is done with this one, which keeps the footprint small
+  // enough for four or five workgroups per CU.
+  __shared__ __attribute__((aligned(16))) float xs[NPIX * PS];
+  __shared__ __attribute__((aligned(16))) float ws[BN * WS];
   __shared__ double red[4][BN][2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4;
@@ -180,13 +183,13 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       }
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&]() {
 #pragma unroll
     for (int u = 0; u < NXT; ++u) {
       const int e = tid + u * 256;
       if (NX % 256 == 0 || e < NX) {
         const int c4 = e / NPIX, pix = e - c4 * NPIX;
-        *reinterpret_cast<v4f*>(&xs[buf][pix * PS + 4 * c4]) = rx[u];
+        *reinterpret_cast<v4f*>(&xs[pix * PS + 4 * c4]) = rx[u];
       }
     }
 #pragma unroll
@@ -205,7 +208,7 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
           tap = rem / C4;
           c4 = rem - tap * C4;
         }
-        *reinterpret_cast<v4f*>(&ws[buf][row * WS + tap * CC + 4 * c4]) = rw[u];
+        *reinterpret_cast<v4f*>(&ws[row * WS + tap * CC + 4 * c4]) = rw[u];
       }
     }
   };
@@ -222,14 +225,10 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   const int wbase = (lane & 15) * WS + 4 * kq;
 
   // Epilogue operands of the data gradient (ReLU mask, the next batch
-  // norm's x and y), loaded together with the inputs of the tile before, so
-  // their latency overlaps a whole tile: four consecutive pixels of one
-  // channel per lane and block.
-  // With 32-channel tiles a second set does not fit in the registers: those
-  // load the operands just before the tile's last MFMAs instead.
-  constexpr bool AHEAD = FLIP && TN == 1;
-  v4f e_mask[TM][TN], e_x[TM][TN], e_y[TM][TN];     // this tile's
-  v4f n_mask[TM][TN], n_x[TM][TN], n_y[TM][TN];     // the next tile's (AHEAD)
+  // norm's x and y), four consecutive pixels of one channel per lane and
+  // block, are loaded before the tile's last chunk of MFMAs, so their
+  // latency overlaps that chunk.
+  v4f e_mask[TM][TN], e_x[TM][TN], e_y[TM][TN];
   auto gofs = [&](const Tile& d, int t, int u) {  // (plane offset, first pixel)
     const int co = d.co0 + u * 16 + (lane & 15);
     const int p0 = d.oh0 * WW + (wave * TM + t) * 16 + 4 * kq;
@@ -346,10 +345,8 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   int t = blockIdx.x;
   Tile d = decode(t);
   load(d, 0);
-  if (AHEAD) prefetch_epilogue(d, e_mask, e_x, e_y);
-  store(0);
+  store();
   __syncthreads();
-  int cur = 0;
   while (true) {
 #pragma unroll
     for (int x = 0; x < TM; ++x)
@@ -361,12 +358,9 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       const bool last = c + 1 == nchunk;
       const bool has_next = !last || more;
       if (has_next) load(last ? dn : d, last ? 0 : (c + 1) * CC);
-      // the next tile's epilogue operands go out with its inputs, a whole
-      // tile ahead of their use
-      if (AHEAD && last && more) prefetch_epilogue(dn, n_mask, n_x, n_y);
-      if (!AHEAD && last) prefetch_epilogue(d, e_mask, e_x, e_y);
-      const float* X = xs[cur];
-      const float* Wl = ws[cur];
+      if (last) prefetch_epilogue(d, e_mask, e_x, e_y);
+      const float* X = xs;
+      const float* Wl = ws;
 #pragma unroll TAP_UNROLL
       for (int tap = 0; tap < 9; ++tap) {
         const int r = tap / 3, s = tap - r * 3;
@@ -388,24 +382,16 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
               for (int u = 0; u < TN; ++u) acc[x][u] = mfma4(av[x][q], bv[u][q], acc[x][u]);
         }
       }
-      if (has_next) store(cur ^ 1);
+      if (has_next) {
+        __syncthreads();
+        store();
+      }
       __syncthreads();
-      cur ^= 1;
     }
     epilogue(d);
     if (!more) break;
     t += G;
     d = dn;
-    if (AHEAD) {
-#pragma unroll
-      for (int x = 0; x < TM; ++x)
-#pragma unroll
-        for (int y = 0; y < TN; ++y) {
-          e_mask[x][y] = n_mask[x][y];
-          e_x[x][y] = n_x[x][y];
-          e_y[x][y] = n_y[x][y];
-        }
-    }
   }
 }
 
