@@ -718,13 +718,14 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
 #pragma unroll
   for (int t = 0; t < 9; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  for (int u = u0; u < u1; ++u) {
+  // Unit u's tiles go to registers while the unit before it computes.
+  v4f ra[NA4T];
+  float rx[NXT];
+  auto load = [&](int u) {
     const int img = u / tiles_img, h0 = (u - img * tiles_img) * TH;
     const int n = j * a.b + img;
     const float* DY = a.dy + ((int64_t)n * a.Co + co0) * HW + h0 * WW;
     const float* X = a.x + ((int64_t)n * a.Ci + ci0) * HW;
-    v4f ra[NA4T];
-    float rx[NXT];
 #pragma unroll
     for (int i = 0; i < NA4T; ++i) {
       const int e = tid + i * 256;
@@ -743,7 +744,8 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
                       (unsigned)iw < (unsigned)WW;
       rx[i] = buf_ld(xsrc, ok ? (uint32_t)((c * HW + ih * WW + iw) * 4) : OUTSIDE);
     }
-    __syncthreads();  // the previous unit's reads of the tiles are done
+  };
+  auto store = [&]() {
 #pragma unroll
     for (int i = 0; i < NA4T; ++i) {
       const int e = tid + i * 256;
@@ -764,7 +766,14 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
         Bs[c * SB + rem] = rx[i];
       }
     }
+  };
+
+  if (u0 < u1) load(u0);
+  for (int u = u0; u < u1; ++u) {
+    __syncthreads();  // the previous unit's reads of the tiles are done
+    store();
     __syncthreads();
+    if (u + 1 < u1) load(u + 1);
 #pragma unroll 2
     for (int i = 0; i < QW; ++i) {
       const int q = wave + 4 * i;
@@ -907,12 +916,14 @@ hipError_t dispatch(const DirectArgs& a, int W, hipStream_t s, const char** name
   return dispatch_w<FLIP, 8>(a, t, s, name);
 }
 
-// Weight gradient: units of 8 rows; the split gives every CU two
-// workgroups over all replicas and channel blocks where the units allow.
-constexpr int WG_TH = 8;
+// Weight gradient: units of 4 rows (8 at width 8), so that a workgroup
+// has several units to pipeline; the split gives every CU two workgroups
+// over all replicas and channel blocks where the units allow.
+constexpr int WG_TH32 = 4, WG_TH16 = 4, WG_TH8 = 8;
+int wgrad_th(int W) { return W == 32 ? WG_TH32 : W == 16 ? WG_TH16 : WG_TH8; }
 
 void wgrad_split(const ConvGeom& g, int* splits, int* per) {
-  const int units = g.b * (g.H / WG_TH);
+  const int units = g.b * (g.H / wgrad_th(g.W));
   const int64_t blocks = (int64_t)g.k * (g.Co / 16) * (g.Ci / 16);
   int sp = (int)std::max<int64_t>(1, std::min<int64_t>(units, (DIRECT_MIN_WGS + blocks - 1) / blocks));
   const int pr = (units + sp - 1) / sp;
@@ -964,9 +975,9 @@ hipError_t conv_direct_wgrad(const ConvBwdWeightArgs& w, hipStream_t s, const ch
   a.x = w.x; a.dy = w.dy; a.dw = w.dw; a.pstride = w.pstride; a.partial = w.partial;
   wgrad_split(w.g, &a.splits, &a.per);
   if (w.splits != a.splits) return hipErrorInvalidValue;  // scratch sized for another split
-  if (w.g.W == 32) return launch_wgrad<32, WG_TH>(a, s, name);
-  if (w.g.W == 16) return launch_wgrad<16, WG_TH>(a, s, name);
-  return launch_wgrad<8, WG_TH>(a, s, name);
+  if (w.g.W == 32) return launch_wgrad<32, WG_TH32>(a, s, name);
+  if (w.g.W == 16) return launch_wgrad<16, WG_TH16>(a, s, name);
+  return launch_wgrad<8, WG_TH8>(a, s, name);
 }
 
 bool conv_direct_fwd_ok(const ConvGeom& g) {
