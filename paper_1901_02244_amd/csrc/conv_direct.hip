@@ -25,9 +25,6 @@
 #include <algorithm>
 #include <string>
 
-#ifndef TAP_UNROLL
-#define TAP_UNROLL 9
-#endif
 
 namespace cbk {
 namespace {
@@ -49,6 +46,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const float* base, ui
 }
 __device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t off_bytes) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off_bytes, 0, 0));
+}
+
+// Workgroups are handed to the eight XCDs in turn (workgroup w to XCD
+// w % 8).  Renumbering them XCD-major gives the workgroups of one XCD a
+// contiguous range of ids, so the neighbouring tiles they take share halo
+// rows and filters in that XCD's L2.  A bijection on [0, G) for any G.
+constexpr int NXCD = 8;
+__device__ __forceinline__ int xcd_major(int w, int G) {
+  const int x = w % NXCD, i = w / NXCD, q = G / NXCD, r = G % NXCD;
+  return x * q + min(x, r) + i;
 }
 
 // Channel stride of the LDS input tile, rounded so that the four lane groups
@@ -342,7 +349,7 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   // Workgroup w takes tiles w, w + G, w + 2G, ...  Every (tile, chunk) item
   // prefetches the next item's inputs into registers before its MFMAs.
   const int G = gridDim.x;
-  int t = blockIdx.x;
+  int t = xcd_major(blockIdx.x, G);
   Tile d = decode(t);
   load(d, 0);
   store();
@@ -361,7 +368,7 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       if (last) prefetch_epilogue(d, e_mask, e_x, e_y);
       const float* X = xs;
       const float* Wl = ws;
-#pragma unroll TAP_UNROLL
+#pragma unroll
       for (int tap = 0; tap < 9; ++tap) {
         const int r = tap / 3, s = tap - r * 3;
         const int tw = FLIP ? 8 - tap : tap;

@@ -38,7 +38,7 @@ __device__ __forceinline__ void st(v4f* p, v4f v) {
 template <int R, bool CORRECT, bool LMOM, bool NT>
 __global__ __launch_bounds__(256) void sma_k(SMAArgs a) {
   constexpr int C = 64 / R;  // float4 columns per wave
-  constexpr int U = 4;       // replicas loaded before any is updated
+  constexpr int U = 2;       // replicas loaded before any is updated
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane / C, col = lane - r * C;
   const int64_t e = ((int64_t)blockIdx.x * 4 + wave) * C + col;
