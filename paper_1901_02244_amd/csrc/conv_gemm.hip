@@ -161,6 +161,7 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
 
   const float* bias = a.bias ? a.bias + (int64_t)j * a.pstride : nullptr;
   float* Y = a.y + (int64_t)j * g.b * N * HoWo;
+  const bool vec = (HoWo & 3) == 0 && (reinterpret_cast<uintptr_t>(Y) & 15) == 0;
   double s1[TN], s2[TN];  // per-column sums of the stored outputs (BN statistics)
 #pragma unroll
   for (int y = 0; y < TN; ++y) s1[y] = s2[y] = 0.0;
@@ -173,6 +174,20 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
       if (n >= N || mb >= M) continue;
       const float bv = bias ? bias[n] : 0.f;
       int img = mb / HoWo, p = mb - img * HoWo;
+      if (vec) {
+        // the lane's four pixels are consecutive in one plane
+        v4f v = acc[x][y];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float e = v[i] + bv;
+          if (a.relu) e = relu0(e);
+          v[i] = e;
+          s1[y] += (double)e;
+          s2[y] += (double)e * e;
+        }
+        *reinterpret_cast<v4f*>(&Y[((int64_t)img * N + n) * HoWo + p]) = v;
+        continue;
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         if (mb + i < M) {
@@ -339,6 +354,12 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   const bool bn = a.bn_part != nullptr;
   const float* BX = bn ? a.bn_x + (int64_t)j * g.b * N * HW : nullptr;
   const float* BY = (bn && a.bn_y) ? a.bn_y + (int64_t)j * g.b * N * HW : nullptr;
+  // float4 epilogue when a lane's four pixels never straddle two planes and
+  // every tensor it touches per pixel is 16-byte aligned
+  const uintptr_t align = reinterpret_cast<uintptr_t>(DX) | reinterpret_cast<uintptr_t>(MSK) |
+                          reinterpret_cast<uintptr_t>(BX) | reinterpret_cast<uintptr_t>(BY) |
+                          (a.add_mode == ADD_SAME ? reinterpret_cast<uintptr_t>(ADD) : 0);
+  const bool vec = (HW & 3) == 0 && (align & 15) == 0;
   double s1[TN], s2[TN];
 #pragma unroll
   for (int y = 0; y < TN; ++y) s1[y] = s2[y] = 0.0;
@@ -354,6 +375,42 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       if (bn) {
         bm = a.bn_mean[j * N + n];
         bi = a.bn_istd[j * N + n];
+      }
+      if (vec) {
+        // the lane's four pixels are consecutive in one plane: float4 access
+        const int64_t idx = ((int64_t)img * N + n) * HW + p;
+        v4f v = acc[x][y];
+        if (a.accumulate) v += *reinterpret_cast<const v4f*>(DX + idx);
+        if (a.add_mode == ADD_SAME) {
+          v += *reinterpret_cast<const v4f*>(ADD + idx);
+        } else if (a.add_mode == ADD_SUBSAMPLE) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int pp = p + i, ih = pp / g.W, iw = pp - ih * g.W;
+            if (ih % a.add_st == 0 && iw % a.add_st == 0)
+              v[i] += ADD[(((int64_t)img * a.add_C + n) * Hs + ih / a.add_st) * Ws + iw / a.add_st];
+          }
+        }
+        if (MSK) {
+          const v4f mk = *reinterpret_cast<const v4f*>(MSK + idx);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (!(mk[i] > 0.f)) v[i] = 0.f;
+        }
+        *reinterpret_cast<v4f*>(DX + idx) = v;
+        if (bn) {
+          const v4f bx = *reinterpret_cast<const v4f*>(BX + idx);
+          v4f by = {1.f, 1.f, 1.f, 1.f};
+          if (BY) by = *reinterpret_cast<const v4f*>(BY + idx);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float d = (BY && !(by[i] > 0.f)) ? 0.f : v[i];
+            const float xh = (bx[i] - bm) * bi;
+            s1[y] += (double)d;
+            s2[y] += (double)d * xh;
+          }
+        }
+        continue;
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
