@@ -178,6 +178,19 @@ int cb_set_learners(cb_ctx* c, int k, float alpha);
 /* The number of active learners. */
 int cb_learners(const cb_ctx* c);
 
+/* Graph replay of cb_step (on != 0) or direct launches (on == 0, the
+ * default).  With replay on, the first cb_step on a given (inputs_dev,
+ * labels_dev) pair captures its forward/backward launches from the
+ * context's stream into a HIP graph; later steps on the same pair launch
+ * that graph, so the host submits one graph instead of each kernel.
+ * Results are bitwise those of direct launches.  The buffers themselves
+ * are read at replay time, so their contents may change between steps; a
+ * graph is kept per pair, at most 8 (the oldest is dropped, after the
+ * stream drains).  cb_set_learners drops all graphs; instrumented steps
+ * (cb_profile_enable) always launch directly.  Switching off drops all
+ * graphs.  Not part of Algorithm 1: launch overhead only. */
+int cb_set_graphs(cb_ctx* c, int on);
+
 /* Algorithm 2 (Sec. 3.4), one observation for one GPU: l learners gave
  * throughput t and t_prev was observed before.  Returns l + 1 if t - t_prev
  * exceeds threshold (but at most l_max), l - 1 if t < t_prev (but at least

@@ -34,7 +34,7 @@ EXPORTS = (
     "cb_test_conv_scratch_bytes", "cb_test_conv", "cb_test_bn_scratch_bytes", "cb_test_bn_fwd",
     "cb_test_bn_bwd", "cb_test_maxpool", "cb_test_softmax_xent",
     "cb_set_lr", "cb_restart", "cb_set_learners", "cb_learners", "cb_tuner_next",
-    "cb_test_conv_dgrad_parts", "cb_test_conv_dgrad",
+    "cb_test_conv_dgrad_parts", "cb_test_conv_dgrad", "cb_set_graphs",
 )
 
 
@@ -108,6 +108,7 @@ def lib():
         L.cb_restart.argtypes = [_P]
         L.cb_set_learners.argtypes = [_P, _i, ctypes.c_float]
         L.cb_learners.argtypes = [_P]
+        L.cb_set_graphs.argtypes = [_P, _i]
         L.cb_tuner_next.argtypes = [_i, ctypes.c_double, ctypes.c_double, ctypes.c_double, _i]
         _lib = L
     return _lib
@@ -223,6 +224,10 @@ class Context:
         self._check(lib().cb_set_learners(self._c, k, alpha), "cb_set_learners")
         self.k = lib().cb_learners(self._c)
         return 0
+
+    def cb_set_graphs(self, on=True):
+        """Replay each step's launches as a HIP graph per input buffer pair."""
+        return self._check(lib().cb_set_graphs(self._c, 1 if on else 0), "cb_set_graphs")
 
     def cb_get_central(self):
         out = np.empty(self.P, dtype=np.float32)

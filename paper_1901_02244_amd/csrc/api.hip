@@ -451,8 +451,35 @@ struct cb_ctx {
   hipStream_t side = nullptr;
   std::vector<hipEvent_t> fork_ev;  // per operator (conv layers only)
   hipEvent_t join_ev = nullptr;
+  // Graph replay: the launches of one forward/backward pass, captured once
+  // per (inputs, labels) pair as a HIP graph and replayed by later steps on
+  // the same buffers; the host then submits one graph instead of every
+  // kernel.  Least recently captured graphs are dropped beyond
+  // GRAPH_CACHE pairs.
+  static constexpr size_t GRAPH_CACHE = 8;
+  struct StepGraph {
+    const void* x;
+    const void* y;
+    hipGraph_t g;
+    hipGraphExec_t e;
+  };
+  bool graphs = false;
+  std::vector<StepGraph> step_graphs;
+  hipStream_t cap = nullptr;  // capture stream (default priority)
+
+  void drop_graphs() {
+    if (step_graphs.empty()) return;
+    (void)hipStreamSynchronize(stream);
+    for (auto& sg : step_graphs) {
+      (void)hipGraphExecDestroy(sg.e);
+      (void)hipGraphDestroy(sg.g);
+    }
+    step_graphs.clear();
+  }
 
   ~cb_ctx() {
+    drop_graphs();
+    if (cap) (void)hipStreamDestroy(cap);
     if (side) {
       (void)hipStreamSynchronize(side);
       (void)hipStreamDestroy(side);
@@ -548,9 +575,8 @@ struct ProfScope {
     ps_.done(nm_, flops, bytes);               \
   } while (0)
 
-int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels) {
+int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s) {
   const Plan& p = c->p;
-  hipStream_t s = c->stream;
   const int k = p.k, b = p.b, N = k * b;
   auto act = [&](int t) -> float* { return t == p.input ? const_cast<float*>(x) : c->at<float>(p.t[t].act); };
   auto grd = [&](int t) -> float* { return c->at<float>(p.t[t].grad); };
@@ -768,6 +794,45 @@ int enqueue_sma(cb_ctx* c, const float* G, int64_t gstride, int correct) {
   return CB_OK;
 }
 
+// One forward/backward pass as a graph replay on the context's stream: the
+// graph of this (inputs, labels) pair if there is one, else the pass
+// captured and instantiated first.  The capture runs on a stream of the
+// library's own (the caller's may be the null stream, which cannot be
+// captured); the side stream joins the capture through the fork events and
+// is joined back before it ends.  Capturing launches nothing.
+int replay_step(cb_ctx* c, const float* x, const int32_t* labels) {
+  for (auto& sg : c->step_graphs)
+    if (sg.x == x && sg.y == labels) {
+      CB_HIP(c, hipGraphLaunch(sg.e, c->stream));
+      return CB_OK;
+    }
+  if (c->step_graphs.size() >= cb_ctx::GRAPH_CACHE) {
+    CB_HIP(c, hipStreamSynchronize(c->stream));
+    (void)hipGraphExecDestroy(c->step_graphs.front().e);
+    (void)hipGraphDestroy(c->step_graphs.front().g);
+    c->step_graphs.erase(c->step_graphs.begin());
+  }
+  if (!c->cap) CB_HIP(c, hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking));
+  CB_HIP(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeRelaxed));
+  const int rc = enqueue_step(c, x, labels, c->cap);
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(c->cap, &g);  // ends the capture on every path
+  if (rc != CB_OK) {
+    if (g) (void)hipGraphDestroy(g);
+    return rc;
+  }
+  CB_HIP(c, e);
+  hipGraphExec_t ex = nullptr;
+  const hipError_t ei = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+  if (ei != hipSuccess) {
+    (void)hipGraphDestroy(g);
+    CB_HIP(c, ei);
+  }
+  c->step_graphs.push_back(cb_ctx::StepGraph{x, labels, g, ex});
+  CB_HIP(c, hipGraphLaunch(ex, c->stream));
+  return CB_OK;
+}
+
 int check_finite(cb_ctx* c) {
   int* flag = c->at<int>(c->p.off_flag);
   CB_HIP(c, zero_ints(flag, 1, c->stream));
@@ -928,7 +993,8 @@ int cb_step(cb_ctx* c, const float* inputs_dev, const int32_t* labels_dev) {
     rc = enqueue_sma(c, c->G(), c->p.Pp, 0);  // unsynced gradient: local step
     if (rc) return rc;
   }
-  rc = enqueue_step(c, inputs_dev, labels_dev);
+  rc = (c->graphs && !c->prof) ? replay_step(c, inputs_dev, labels_dev)
+                               : enqueue_step(c, inputs_dev, labels_dev, c->stream);
   if (rc) return rc;
   c->pending = true;
   return CB_OK;
@@ -1070,6 +1136,7 @@ int cb_set_learners(cb_ctx* c, int k, float alpha) {
       CB_HIP(c, hipMemcpyAsync(c->Wprev() + (int64_t)j * c->p.Pp, c->Z(), pb,
                                hipMemcpyDeviceToDevice, c->stream));
   }
+  c->drop_graphs();  // captured with the old plan
   c->p = std::move(np);
   c->alpha = alpha;
   build_split_tables(c);
@@ -1082,6 +1149,14 @@ int cb_tuner_next(int l, double t, double t_prev, double threshold, int l_max) {
   if (t - t_prev > threshold) return l < l_max ? l + 1 : l;
   if (t < t_prev && l > 1) return l - 1;
   return l;
+}
+
+int cb_set_graphs(cb_ctx* c, int on) {
+  int rc = enter(c);
+  if (rc) return rc;
+  c->graphs = on != 0;
+  if (!c->graphs) c->drop_graphs();
+  return CB_OK;
 }
 
 int cb_profile_enable(cb_ctx* c, int on) {

@@ -14,8 +14,9 @@ namespace cbk {
 // Per-launch timing.  When armed, the next kernel launch on this thread
 // passes the two events to hipExtLaunchKernel, which stamps them on the
 // kernel's own dispatch: the interval is the kernel alone, with no marker
-// packets added around it.  Every kernel of this library goes through
-// klaunch.
+// packets added around it.  Unarmed launches are plain kernel launches,
+// which a stream capture records as graph nodes.  Every kernel of this
+// library goes through klaunch.
 struct LaunchTiming {
   hipEvent_t start = nullptr, stop = nullptr;
 };
@@ -26,7 +27,10 @@ inline void klaunch(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t shm, h
                     A... args) {
   const LaunchTiming t = g_launch_timing;
   g_launch_timing = LaunchTiming();
-  hipExtLaunchKernelGGL(kernel, grid, block, shm, s, t.start, t.stop, 0u, args...);
+  if (t.start)
+    hipExtLaunchKernelGGL(kernel, grid, block, shm, s, t.start, t.stop, 0u, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, shm, s, args...);
 }
 
 // Geometry of one convolution layer (an FC layer is a 1x1 conv on a 1x1

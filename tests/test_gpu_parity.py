@@ -527,6 +527,52 @@ def test_runs_are_bitwise_reproducible():
     np.testing.assert_array_equal(outs[0][1], outs[1][1])
 
 
+def test_graph_replay_is_bitwise_direct():
+    """Steps replayed from captured HIP graphs give bitwise the results of
+    direct launches, checked after every replay: with synchronisations and
+    unsynchronised (local) steps, the program's own GPU work between
+    replays, an input changed in place (graphs read their buffers at replay
+    time) and a change of the learner count (which drops the graphs)."""
+    m = cb.model("resnet32", 3, 32, 32, 10)
+    w0 = wl.init_w0(cb.cb_tensor_layout(m), 11)
+    k, b = 2, 8
+    direct = cb.Context(m, k, b, 0.5, 0.01, 0.9, w0)
+    graph = cb.Context(m, k, b, 0.5, 0.01, 0.9, w0)
+    graph.cb_set_graphs(True)
+    ring = [tuple(_dev(a) for a in wl.batch(k * b, 3, 32, 32, 10, 11, t)) for t in range(3)]
+
+    def check(tag):
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(direct.cb_get_central(), graph.cb_get_central(), err_msg=tag)
+        np.testing.assert_array_equal(direct.cb_get_loss(), graph.cb_get_loss(), err_msg=tag)
+        for j in range(direct.k):
+            np.testing.assert_array_equal(direct.cb_get_grad(j), graph.cb_get_grad(j),
+                                          err_msg=f"{tag}, gradient of learner {j}")
+
+    def both(x, y, sync=True):
+        for ctx in (direct, graph):
+            ctx.cb_step(x, y)
+            if sync:
+                ctx.cb_sync()
+
+    for it in range(8):
+        x, y = ring[it % 3]
+        both(x, y, sync=it % 3 != 1)
+        # unrelated work of the program between replays
+        torch.randn(4096, device="cuda").sum().item()
+        check(f"iteration {it}")
+    ring[0][0].mul_(0.5)
+    both(*ring[0])
+    check("input changed in place")
+    for ctx in (direct, graph):
+        ctx.cb_set_learners(1, 1.0)
+    for it in range(3):
+        both(ring[1][0][: b], ring[1][1][: b])
+        check(f"one learner, iteration {it}")
+    direct.close()
+    graph.close()
+
+
 # ------------------------------------------------------------ error paths
 
 def test_error_paths():
