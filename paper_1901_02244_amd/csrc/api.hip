@@ -741,6 +741,10 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
             d.bn_y = bn.relu ? act(bn.out) : nullptr;
             d.bn_mean = c->at<float>(bn.mean);
             d.bn_istd = c->at<float>(bn.istd);
+            // When that ReLU output is this layer's input, the ReLU mask has
+            // already zeroed dX wherever it is not positive: the batch norm's
+            // own ReLU test would repeat it on the same tensor.
+            if (d.bn_y == d.mask) d.bn_y = nullptr;
           }
           ProfScope ps(c);
           const char* nm = "conv_bwd_data_k";

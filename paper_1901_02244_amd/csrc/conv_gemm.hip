@@ -29,6 +29,7 @@ namespace cbk {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 constexpr int OUT_OF_RANGE = -(1 << 29);
 
 __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
@@ -236,8 +237,14 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
 }
 
 // ------------------------------------------------------------ data grad
-template <int BM, int BN, int WM, int WN, int R, int ST, int BK>
+// SP (1x1, stride 2, even H and W): only the dX pixels (2oh, 2ow) receive a
+// contribution, so the GEMM runs over the Ho x Wo grid (a quarter of the
+// MFMA work) and the epilogue writes the 2x2 block of each grid point: the
+// contraction at (2oh, 2ow), zero at the other three, every pixel through
+// the same accumulate / add / mask / batch-norm epilogue.
+template <int BM, int BN, int WM, int WN, int R, int ST, int BK, bool SP = false>
 __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
+  static_assert(!SP || (R == 1 && ST == 2), "the grid-only form is the 1x1 stride-2 case");
   constexpr int RS = R * R;
   constexpr int LDK = BK + 4;
   constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
@@ -253,7 +260,7 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int j = blockIdx.z;
   const int HW = g.H * g.W, HoWo = g.Ho * g.Wo;
-  const int M = g.b * HW, N = g.Ci, K = g.Co * RS;
+  const int M = SP ? g.b * HoWo : g.b * HW, N = g.Ci, K = g.Co * RS;
   const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
   const float* DY = a.dy + (int64_t)j * g.b * g.Co * HoWo;
   const float* Wt = a.w + (int64_t)j * a.pstride;
@@ -264,10 +271,16 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   {
     const int m = m0 + am;
     if (m < M) {
-      const int img = m / HW, p = m - img * HW, ih = p / g.W, iw = p - ih * g.W;
-      thp = ih + g.pad;
-      twp = iw + g.pad;
-      yb = img * g.Co * HoWo;
+      if (SP) {  // m is a grid point: dY pixel m % HoWo of image m / HoWo
+        const int img = m / HoWo;
+        thp = twp = 0;
+        yb = img * g.Co * HoWo + (m - img * HoWo);
+      } else {
+        const int img = m / HW, p = m - img * HW, ih = p / g.W, iw = p - ih * g.W;
+        thp = ih + g.pad;
+        twp = iw + g.pad;
+        yb = img * g.Co * HoWo;
+      }
     }
   }
   float ra[KPT];
@@ -278,7 +291,9 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
     for (int i = 0; i < KPT; ++i) {
       const int k = k0 + akq * KPT + i;  // wave-uniform
       float v = 0.f;
-      if (k < K) {
+      if (SP) {
+        if (k < K && thp == 0) v = DY[yb + k * HoWo];
+      } else if (k < K) {
         const int co = k / RS, rs = k - co * RS, r = rs / R, s = rs - r * R;
         const int th = thp - r, tw = twp - s;
         if (ST == 1) {
@@ -375,6 +390,50 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       if (bn) {
         bm = a.bn_mean[j * N + n];
         bi = a.bn_istd[j * N + n];
+      }
+      if (SP) {
+        // grid point m: dX rows 2oh and 2oh + 1, columns 2ow and 2ow + 1,
+        // two pixels (8 bytes) per row
+        for (int i = 0; i < 4 && mb + i < M; ++i) {
+          const int m = mb + i, im = m / HoWo, pp = m - im * HoWo, oh = pp / g.Wo, ow = pp - oh * g.Wo;
+#pragma unroll
+          for (int r2 = 0; r2 < 2; ++r2) {
+            const int ih = 2 * oh + r2;
+            const int64_t idx = (((int64_t)im * N + n) * g.H + ih) * g.W + 2 * ow;
+            v2f v = {r2 == 0 ? acc[x][y][i] : 0.f, 0.f};
+            if (a.accumulate) v += *reinterpret_cast<const v2f*>(DX + idx);
+            if (a.add_mode == ADD_SAME) {
+              v += *reinterpret_cast<const v2f*>(ADD + idx);
+            } else if (a.add_mode == ADD_SUBSAMPLE) {
+#pragma unroll
+              for (int c2 = 0; c2 < 2; ++c2) {
+                const int iw = 2 * ow + c2;
+                if (ih % a.add_st == 0 && iw % a.add_st == 0)
+                  v[c2] += ADD[(((int64_t)im * a.add_C + n) * Hs + ih / a.add_st) * Ws + iw / a.add_st];
+              }
+            }
+            if (MSK) {
+              const v2f mk = *reinterpret_cast<const v2f*>(MSK + idx);
+#pragma unroll
+              for (int c2 = 0; c2 < 2; ++c2)
+                if (!(mk[c2] > 0.f)) v[c2] = 0.f;
+            }
+            *reinterpret_cast<v2f*>(DX + idx) = v;
+            if (bn) {
+              const v2f bx = *reinterpret_cast<const v2f*>(BX + idx);
+              v2f by = {1.f, 1.f};
+              if (BY) by = *reinterpret_cast<const v2f*>(BY + idx);
+#pragma unroll
+              for (int c2 = 0; c2 < 2; ++c2) {
+                const float d = (BY && !(by[c2] > 0.f)) ? 0.f : v[c2];
+                const float xh = (bx[c2] - bm) * bi;
+                s1[y] += (double)d;
+                s2[y] += (double)d * xh;
+              }
+            }
+          }
+        }
+        continue;
       }
       if (vec) {
         // the lane's four pixels are consecutive in one plane: float4 access
@@ -695,12 +754,14 @@ inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b);
 // Name of one kernel instantiation, as the profiler shows its template.
 template <int KIND, int BM, int BN, int WM, int WN, int R, int ST, int BK>
 const char* tile_name() {
-  static const char* base[3] = {"conv_fwd_k", "conv_bwd_data_k", "conv_bwd_weight_k"};
+  // KIND 3: the grid-only data gradient (SP = true)
+  static const char* base[4] = {"conv_fwd_k", "conv_bwd_data_k", "conv_bwd_weight_k",
+                                "conv_bwd_data_k"};
   static const std::string n = std::string(base[KIND]) + "<" + std::to_string(BM) + ", " +
                                std::to_string(BN) + ", " + std::to_string(WM) + ", " +
                                std::to_string(WN) + ", " + std::to_string(R) +
                                (ST ? ", " + std::to_string(ST) : "") + ", " +
-                               std::to_string(BK) + ">";
+                               std::to_string(BK) + (KIND == 3 ? ", true>" : ">");
   return n.c_str();
 }
 
@@ -718,13 +779,13 @@ hipError_t launch_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int R, int ST>
+template <int BM, int BN, int WM, int WN, int R, int ST, bool SP = false>
 hipError_t launch_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
   constexpr int BK = stage_k<BM>();
-  const int M = a.g.b * a.g.H * a.g.W;
+  const int M = SP ? a.g.b * a.g.Ho * a.g.Wo : a.g.b * a.g.H * a.g.W;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Ci, BN), a.g.k);
-  klaunch((conv_bwd_data_k<BM, BN, WM, WN, R, ST, BK>), grid, dim3(256), 0, s, a);
-  if (name) *name = tile_name<1, BM, BN, WM, WN, R, ST, BK>();
+  klaunch((conv_bwd_data_k<BM, BN, WM, WN, R, ST, BK, SP>), grid, dim3(256), 0, s, a);
+  if (name) *name = SP ? tile_name<3, BM, BN, WM, WN, R, ST, BK>() : tile_name<1, BM, BN, WM, WN, R, ST, BK>();
   return hipGetLastError();
 }
 
@@ -771,16 +832,24 @@ hipError_t fwd_r(const ConvFwdArgs& a, hipStream_t s, const char** name) {
   }
 }
 
-template <int R, int ST>
+template <int R, int ST, bool SP = false>
 hipError_t bwd_data_r(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
-  switch (pick_tile((int64_t)a.g.b * a.g.H * a.g.W, a.g.Ci, a.g.k)) {
-    case 0: return launch_bwd_data<256, 16, 4, 1, R, ST>(a, s, name);
-    case 1: return launch_bwd_data<64, 16, 4, 1, R, ST>(a, s, name);
-    case 2: return launch_bwd_data<128, 32, 4, 1, R, ST>(a, s, name);
-    case 3: return launch_bwd_data<64, 32, 4, 1, R, ST>(a, s, name);
-    case 4: return launch_bwd_data<128, 64, 2, 2, R, ST>(a, s, name);
-    default: return launch_bwd_data<64, 64, 2, 2, R, ST>(a, s, name);
+  const int64_t M = SP ? (int64_t)a.g.b * a.g.Ho * a.g.Wo : (int64_t)a.g.b * a.g.H * a.g.W;
+  switch (pick_tile(M, a.g.Ci, a.g.k)) {
+    case 0: return launch_bwd_data<256, 16, 4, 1, R, ST, SP>(a, s, name);
+    case 1: return launch_bwd_data<64, 16, 4, 1, R, ST, SP>(a, s, name);
+    case 2: return launch_bwd_data<128, 32, 4, 1, R, ST, SP>(a, s, name);
+    case 3: return launch_bwd_data<64, 32, 4, 1, R, ST, SP>(a, s, name);
+    case 4: return launch_bwd_data<128, 64, 2, 2, R, ST, SP>(a, s, name);
+    default: return launch_bwd_data<64, 64, 2, 2, R, ST, SP>(a, s, name);
   }
+}
+
+// The 1x1 stride-2 data gradient on the Ho x Wo grid only (see
+// conv_bwd_data_k): even planes, 8-byte aligned pixel pairs.
+bool s2_grid_ok(const ConvGeom& g) {
+  return g.R == 1 && g.S == 1 && g.st == 2 && g.pad == 0 && g.H % 2 == 0 && g.W % 2 == 0 &&
+         g.Ho == g.H / 2 && g.Wo == g.W / 2;
 }
 
 template <int R>
@@ -795,6 +864,7 @@ hipError_t bwd_weight_r(const ConvBwdWeightArgs& a, hipStream_t s, const char** 
 }  // namespace
 
 inline bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+inline bool al8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7) == 0; }
 
 int conv_fwd_tiles_m(const ConvGeom& g) {
   if (conv_direct_fwd_ok(g)) return conv_direct_fwd_tiles(g);
@@ -805,7 +875,7 @@ int conv_fwd_tiles_m(const ConvGeom& g) {
 int conv_bwd_data_tiles_m(const ConvGeom& g) {
   if (conv_direct_bwd_data_ok(g)) return conv_direct_bwd_data_tiles(g);
   if (conv_s2_dgrad_ok(g)) return conv_s2_dgrad_tiles(g);
-  const int64_t M = (int64_t)g.b * g.H * g.W;
+  const int64_t M = s2_grid_ok(g) ? (int64_t)g.b * g.Ho * g.Wo : (int64_t)g.b * g.H * g.W;
   return (int)cdiv(M, tile_rows(pick_tile(M, g.Ci, g.k)));
 }
 
@@ -875,7 +945,15 @@ hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** n
   const int key = a.g.R * 10 + a.g.st;
   switch (key) {
     case 11: return bwd_data_r<1, 1>(a, s, name);
-    case 12: return bwd_data_r<1, 2>(a, s, name);
+    case 12:
+      if (s2_grid_ok(a.g)) {
+        // the batch-norm partials are laid out for the grid's tiles
+        if (!(al8(a.dx) && al8(a.mask) && al8(a.bn_x) && al8(a.bn_y) &&
+              (a.add_mode != ADD_SAME || al8(a.add))))
+          return hipErrorInvalidValue;
+        return bwd_data_r<1, 2, true>(a, s, name);
+      }
+      return bwd_data_r<1, 2>(a, s, name);
     case 31: return bwd_data_r<3, 1>(a, s, name);
     case 32: return bwd_data_r<3, 2>(a, s, name);
     case 51: return bwd_data_r<5, 1>(a, s, name);

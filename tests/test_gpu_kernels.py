@@ -292,6 +292,9 @@ DGRAD_EPILOGUE = [
     ("s2.w16.same", 1, 3, 16, 16, 32, 3, 2, 1, 0, 1, 1, 16, 0, 0),
     ("gemm.3x3s2.ragged.sub.bn", 2, 3, 7, 13, 19, 3, 2, 1, 1, 1, 2, 19, 1, 1),
     ("gemm.5x5.mask", 2, 4, 6, 14, 16, 5, 1, 0, 0, 1, 0, 0, 1, 1),
+    # 1x1 stride 2 on even planes: the GEMM over the output grid only
+    ("gemm.1x1s2.grid.acc.mask.same.bn", 2, 3, 24, 14, 40, 1, 2, 0, 1, 1, 1, 24, 1, 1),
+    ("gemm.1x1s2.grid.sub.bn", 2, 5, 20, 10, 36, 1, 2, 0, 0, 0, 2, 20, 1, 0),
 ]
 
 
