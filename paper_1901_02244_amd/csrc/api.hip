@@ -644,7 +644,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
       case OP_XENT:
         CB_LAUNCH(c, "softmax_xent_k", 0.0, 4.0 * N * (2.0 * p.m.num_classes + 1),
                   softmax_xent(act(o.in), labels, k, b, p.m.num_classes, grd(o.in),
-                               c->at<float>(p.off_loss), s));
+                               c->at<float>(p.off_loss), s, &nm_));
         break;
     }
   }

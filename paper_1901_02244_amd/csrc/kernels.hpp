@@ -215,7 +215,8 @@ hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t
                    const char** name = nullptr);
 // Mean softmax cross-entropy per replica and its gradient wrt the logits.
 hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b, int classes,
-                        float* dlogits, float* loss, hipStream_t s);
+                        float* dlogits, float* loss, hipStream_t s,
+                        const char** name = nullptr);
 
 // Fused SMA synchronisation (Algorithm 1).  W, G, Wprev are [k][stride];
 // z, zp are [>= P] with P padded to a multiple of 4 elements.

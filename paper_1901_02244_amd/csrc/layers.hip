@@ -469,6 +469,39 @@ __global__ __launch_bounds__(256) void softmax_xent_k(const float* logits, const
   if (threadIdx.x == 0) loss[j] = (float)((((red[0] + red[1]) + red[2]) + red[3]) / b);
 }
 
+// Few classes: one row per thread (a wave per row would spend its time in
+// shuffles and serial latency).  Block j is replica j; rows beyond the block
+// size are taken in further passes.  The replica's loss is the fixed-order
+// sum of the per-row terms (thread order within a wave by xor butterfly,
+// then the four waves in order).
+constexpr int XENT_ROW_CLASSES = 32;
+__global__ __launch_bounds__(256) void softmax_xent_rows_k(const float* logits,
+                                                           const int32_t* labels, int b,
+                                                           int classes, float* dlogits,
+                                                           float* loss) {
+  __shared__ double red[4];
+  const int j = blockIdx.x, w = threadIdx.x >> 6;
+  double tot = 0.0;
+  for (int i = threadIdx.x; i < b; i += 256) {
+    const int64_t row = (int64_t)(j * b + i) * classes;
+    const float* o = logits + row;
+    float mx = -INFINITY;
+    for (int c = 0; c < classes; ++c) mx = fmaxf(mx, o[c]);
+    float se = 0.f;
+    for (int c = 0; c < classes; ++c) se += expf(o[c] - mx);
+    const float lse = mx + logf(se);
+    const int y = labels[j * b + i];
+    const bool yok = (unsigned)y < (unsigned)classes;
+    for (int c = 0; c < classes; ++c)
+      dlogits[row + c] = (expf(o[c] - lse) - (c == y ? 1.f : 0.f)) / b;
+    tot += yok ? (double)(lse - o[y]) : (double)NAN;
+  }
+  tot = wave_sum_d(tot);
+  if ((threadIdx.x & 63) == 0) red[w] = tot;
+  __syncthreads();
+  if (threadIdx.x == 0) loss[j] = (float)((((red[0] + red[1]) + red[2]) + red[3]) / b);
+}
+
 }  // namespace
 
 int bn_chunks(int b, int HW, int C, int k) {
@@ -550,9 +583,15 @@ hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t
 }
 
 hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b, int classes,
-                        float* dlogits, float* loss, hipStream_t s) {
-  klaunch(softmax_xent_k, dim3(k), dim3(256), 0, s, logits, labels, b, classes,
-                     dlogits, loss);
+                        float* dlogits, float* loss, hipStream_t s, const char** name) {
+  if (classes <= XENT_ROW_CLASSES) {
+    if (name) *name = "softmax_xent_rows_k";
+    klaunch(softmax_xent_rows_k, dim3(k), dim3(256), 0, s, logits, labels, b, classes, dlogits,
+            loss);
+  } else {
+    if (name) *name = "softmax_xent_k";
+    klaunch(softmax_xent_k, dim3(k), dim3(256), 0, s, logits, labels, b, classes, dlogits, loss);
+  }
   return hipGetLastError();
 }
 

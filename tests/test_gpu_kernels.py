@@ -258,7 +258,9 @@ def test_maxpool_kernels(case):
 
 
 # (name, k, b, classes)
-XENT = [("lenet", 8, 16, 10), ("r32", 4, 32, 10), ("r50", 2, 32, 1000), ("ragged", 3, 5, 7)]
+XENT = [("lenet", 8, 16, 10), ("r32", 4, 32, 10), ("r50", 2, 32, 1000), ("ragged", 3, 5, 7),
+        # a row per thread up to 32 classes, in several passes beyond 256 rows; a wave per row above
+        ("rows.b300", 2, 300, 10), ("rows.c32", 3, 7, 32), ("waves.c33", 2, 5, 33)]
 
 
 @pytest.mark.parametrize("case", XENT, ids=[c[0] for c in XENT])
