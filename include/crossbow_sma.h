@@ -232,11 +232,13 @@ int cb_test_bn_fwd(int k, int b, int C, int H, int W, int relu, const float* x,
                    void* scratch, size_t scratch_bytes, void* stream);
 
 /* Backward of cb_test_bn_fwd given its mean and istd: dy is masked where
- * mask_y <= 0 (pass the forward output when the ReLU is on, else NULL);
- * dx, and dgamma/dbeta into grads. */
+ * mask_y <= 0 (pass the forward output when the ReLU is on, else NULL), or,
+ * with relu_x (mask_y NULL), where the norm's output recomputed from x,
+ * fmaf(gamma, (x - mean) * istd, beta), is not positive (the forward's
+ * exact decision); dx, and dgamma/dbeta into grads. */
 int cb_test_bn_bwd(int k, int b, int C, int H, int W, const float* x, const float* mask_y,
-                   const float* dy, const float* params, int64_t pstride, const float* mean,
-                   const float* istd, float* dx, float* grads, void* scratch,
+                   int relu_x, const float* dy, const float* params, int64_t pstride,
+                   const float* mean, const float* istd, float* dx, float* grads, void* scratch,
                    size_t scratch_bytes, void* stream);
 
 /* Max pool K x K (first strict maximum wins, padded cells never win) on
@@ -256,7 +258,10 @@ int cb_test_maxpool(int N, int C, int H, int W, int K, int stride, int pad, cons
  * with d = dx where bn_y > 0 (all of dx if bn_y is NULL) and
  * xh = (bn_x - mean) * istd, per replica and channel the partial sums of d
  * and d*xh are written to bn_part [k][Ci][parts][2] (fp64), parts =
- * cb_test_conv_dgrad_parts(); their sum over parts is the total.  Same
+ * cb_test_conv_dgrad_parts(); their sum over parts is the total.  bn_gamma
+ * (optional, with bn_y; gamma and beta at bn_gamma + j*pstride + [0, Ci) and
+ * [Ci, 2Ci)) lets the implicit-GEMM epilogue take bn_y > 0 as
+ * fmaf(gamma, xh, beta) > 0 instead of reading bn_y: bn_y must agree.  Same
  * kernels and tile choices as cb_step; device pointers 16-byte aligned. */
 int cb_test_conv_dgrad_parts(int k, int b, int Ci, int H, int W, int Co, int R, int stride,
                              int pad);
@@ -264,7 +269,8 @@ int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int st
                        const float* dy, const float* params, int64_t pstride, float* dx,
                        int accumulate, const float* mask, const float* add, int add_mode,
                        int add_C, const float* bn_x, const float* bn_y, const float* bn_mean,
-                       const float* bn_istd, double* bn_part, void* stream);
+                       const float* bn_istd, const float* bn_gamma, double* bn_part,
+                       void* stream);
 
 /* Mean softmax cross-entropy of each replica's b rows of logits (Eq. 2),
  * loss [k], and its gradient dlogits [k*b][classes]. */

@@ -97,13 +97,13 @@ def lib():
         L.cb_test_bn_scratch_bytes.argtypes = [_i] * 5
         L.cb_test_bn_fwd.argtypes = [_i] * 6 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P,
                                                 ctypes.c_size_t, _P]
-        L.cb_test_bn_bwd.argtypes = [_i] * 5 + [_P, _P, _P, _P, ctypes.c_int64, _P, _P, _P, _P,
-                                                _P, ctypes.c_size_t, _P]
+        L.cb_test_bn_bwd.argtypes = [_i] * 5 + [_P, _P, _i, _P, _P, ctypes.c_int64, _P, _P, _P,
+                                                _P, _P, ctypes.c_size_t, _P]
         L.cb_test_maxpool.argtypes = [_i] * 7 + [_P, _P, _P, _P, _i, _P, _P]
         L.cb_test_softmax_xent.argtypes = [_i] * 3 + [_P, _P, _P, _P, _P]
         L.cb_test_conv_dgrad_parts.argtypes = [_i] * 9
         L.cb_test_conv_dgrad.argtypes = [_i] * 9 + [_P, _P, ctypes.c_int64, _P, _i, _P, _P, _i, _i,
-                                                    _P, _P, _P, _P, _P, _P]
+                                                    _P, _P, _P, _P, _P, _P, _P]
         L.cb_set_lr.argtypes = [_P, ctypes.c_float]
         L.cb_restart.argtypes = [_P]
         L.cb_set_learners.argtypes = [_P, _i, ctypes.c_float]

@@ -667,7 +667,10 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
         BNBwdArgs a;
         a.k = k; a.b = b; a.C = o.C; a.H = o.H; a.W = o.W;
         a.x = act(o.in);
-        a.y = o.relu ? act(o.out) : nullptr;
+        // without a residual input the ReLU mask is recomputed from x
+        // (read anyway) instead of read from y
+        a.relu_x = o.relu && o.res < 0;
+        a.y = (o.relu && !a.relu_x) ? act(o.out) : nullptr;
         a.dy = grd(o.out);
         a.dx = grd(o.in);
         a.dres = o.res >= 0 ? c->at<float>(o.dres) : nullptr;
@@ -680,7 +683,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
         a.chunks = o.chunks;
         a.parts = o.bwd_parts > 0 ? o.bwd_parts : o.chunks;
         const double n = (double)N * o.C * o.H * o.W;
-        const double mask = o.relu ? 1.0 : 0.0, dres = o.res >= 0 ? 1.0 : 0.0;
+        const double mask = a.y ? 1.0 : 0.0, dres = o.res >= 0 ? 1.0 : 0.0;
         if (o.bwd_parts == 0)
           CB_LAUNCH(c, "bn_bwd_stats_k", 0.0, 4.0 * n * (2.0 + mask), bn_bwd_stats(a, s));
         CB_LAUNCH(c, "bn_bwd_apply_k", 0.0, 4.0 * n * (3.0 + mask + dres), bn_bwd_apply(a, s, &nm_));
@@ -741,6 +744,9 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
             d.bn_y = bn.relu ? act(bn.out) : nullptr;
             d.bn_mean = c->at<float>(bn.mean);
             d.bn_istd = c->at<float>(bn.istd);
+            // without a residual input the norm's ReLU output can be
+            // recomputed from bn_x (the implicit-GEMM epilogue does)
+            if (bn.relu && bn.res < 0) d.bn_gamma = W + bn.g_off;
             // When that ReLU output is this layer's input, the ReLU mask has
             // already zeroed dX wherever it is not positive: the batch norm's
             // own ReLU test would repeat it on the same tensor.

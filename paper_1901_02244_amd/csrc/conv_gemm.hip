@@ -368,7 +368,10 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
                                     : (int64_t)j * g.b * a.add_C * Hs * Ws;
   const bool bn = a.bn_part != nullptr;
   const float* BX = bn ? a.bn_x + (int64_t)j * g.b * N * HW : nullptr;
-  const float* BY = (bn && a.bn_y) ? a.bn_y + (int64_t)j * g.b * N * HW : nullptr;
+  // the norm's ReLU output recomputed from its input where gamma is given
+  // (one tensor fewer to read), else read
+  const float* BG = (bn && a.bn_y && a.bn_gamma) ? a.bn_gamma + (int64_t)j * a.pstride : nullptr;
+  const float* BY = (bn && a.bn_y && !BG) ? a.bn_y + (int64_t)j * g.b * N * HW : nullptr;
   // float4 epilogue when a lane's four pixels never straddle two planes and
   // every tensor it touches per pixel is 16-byte aligned
   const uintptr_t align = reinterpret_cast<uintptr_t>(DX) | reinterpret_cast<uintptr_t>(MSK) |
@@ -386,10 +389,14 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       const int mb = m0 + wm0 + x * 16 + (lane >> 4) * 4;
       if (n >= N || mb >= M) continue;
       int img = mb / HW, p = mb - img * HW;
-      float bm = 0.f, bi = 0.f;
+      float bm = 0.f, bi = 0.f, bg = 0.f, bb = 0.f;
       if (bn) {
         bm = a.bn_mean[j * N + n];
         bi = a.bn_istd[j * N + n];
+      }
+      if (BG) {
+        bg = BG[n];
+        bb = BG[N + n];
       }
       if (SP) {
         // grid point m: dX rows 2oh and 2oh + 1, columns 2ow and 2ow + 1,
@@ -425,7 +432,8 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
               if (BY) by = *reinterpret_cast<const v2f*>(BY + idx);
 #pragma unroll
               for (int c2 = 0; c2 < 2; ++c2) {
-                const float d = (BY && !(by[c2] > 0.f)) ? 0.f : v[c2];
+                const bool on = BY ? by[c2] > 0.f : BG ? bn_affine(bx[c2], bm, bi, bg, bb) > 0.f : true;
+                const float d = on ? v[c2] : 0.f;
                 const float xh = (bx[c2] - bm) * bi;
                 s1[y] += (double)d;
                 s2[y] += (double)d * xh;
@@ -463,7 +471,8 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
           if (BY) by = *reinterpret_cast<const v4f*>(BY + idx);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float d = (BY && !(by[i] > 0.f)) ? 0.f : v[i];
+            const bool on = BY ? by[i] > 0.f : BG ? bn_affine(bx[i], bm, bi, bg, bb) > 0.f : true;
+            const float d = on ? v[i] : 0.f;
             const float xh = (bx[i] - bm) * bi;
             s1[y] += (double)d;
             s2[y] += (double)d * xh;
@@ -487,7 +496,8 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
           if (MSK && !(MSK[idx] > 0.f)) v = 0.f;
           DX[idx] = v;
           if (bn) {
-            const float d = (BY && !(BY[idx] > 0.f)) ? 0.f : v;
+            const bool on = BY ? BY[idx] > 0.f : BG ? bn_affine(BX[idx], bm, bi, bg, bb) > 0.f : true;
+            const float d = on ? v : 0.f;
             const float xh = (BX[idx] - bm) * bi;
             s1[y] += (double)d;
             s2[y] += (double)d * xh;

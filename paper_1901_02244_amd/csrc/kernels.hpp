@@ -64,6 +64,14 @@ struct ConvFwdArgs {
 //     shortcut read backwards; c < Ci <= Csrc).
 enum { ADD_NONE = 0, ADD_SAME = 1, ADD_SUBSAMPLE = 2 };
 
+// A batch norm's output before its residual input and ReLU,
+// gamma * (x - mean) * istd + beta, as one fixed sequence of fp32 operations
+// (a multiply, then a fused multiply-add), so that a backward kernel that
+// recomputes the ReLU decision from x takes exactly the forward's.
+__device__ __forceinline__ float bn_affine(float x, float mean, float istd, float ga, float be) {
+  return __builtin_fmaf(ga, (x - mean) * istd, be);
+}
+
 struct ConvBwdDataArgs {
   ConvGeom g;
   const float* dy;    // [k*b][Co][Ho][Wo]
@@ -76,13 +84,18 @@ struct ConvBwdDataArgs {
   int add_mode, add_C, add_st;
   // If bn_part is not null, dx is the output gradient of a batch norm; the
   // epilogue also writes that norm's backward partial sums per M tile:
-  // with d = dx masked where bn_y <= 0 (bn_y may be null) and
-  // xh = (bn_x - mean) * istd: sum d and sum d*xh, [k][Ci][tiles_m][2].
+  // with d = dx masked where the norm's ReLU output bn_y is not positive
+  // (bn_y null: no mask) and xh = (bn_x - mean) * istd: sum d and sum
+  // d*xh, [k][Ci][tiles_m][2].  For a norm with no residual input the
+  // caller may also give bn_gamma: the implicit-GEMM epilogue then
+  // recomputes the ReLU output as bn_affine of bn_x instead of reading
+  // bn_y (the direct kernels read bn_y).
   double* bn_part;
   const float* bn_x;
   const float* bn_y;
   const float* bn_mean;
   const float* bn_istd;
+  const float* bn_gamma = nullptr;  // replica 0 gamma [Ci], beta at + Ci; pstride apart
 };
 
 struct ConvBwdWeightArgs {
@@ -180,6 +193,7 @@ struct BNBwdArgs {
   int k, b, C, H, W;
   const float* x;       // conv output (BN input)
   const float* y;       // BN output (for the ReLU mask) or nullptr
+  int relu_x = 0;       // y null: the ReLU mask is bn_affine(x) > 0 (no residual input)
   const float* dy;      // gradient at the BN output (before the ReLU mask)
   float* dx;            // gradient at the BN input
   float* dres;          // masked output gradient for the shortcut, or nullptr

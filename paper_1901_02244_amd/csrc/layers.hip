@@ -113,7 +113,7 @@ __global__ __launch_bounds__(256) void bn_apply_k(BNArgs a) {
   ChanIter it(e0 + threadIdx.x, HW);
   for (int e = e0 + threadIdx.x; e < e1; e += 256, it.step(256, HW)) {
     const int64_t off = (int64_t)it.img * a.C * HW + it.p;
-    float v = ga * ((X[off] - mf) * isf) + be;
+    float v = bn_affine(X[off], mf, isf, ga, be);
     if (a.res_mode == RES_SAME) {
       v += a.res[base + off];
     } else if (a.res_mode == RES_SUBSAMPLE) {
@@ -136,6 +136,8 @@ __global__ __launch_bounds__(256) void bn_bwd_stats_k(BNBwdArgs a) {
   const int per = (n + a.chunks - 1) / a.chunks;
   const int e0 = chunk * per, e1 = min(n, e0 + per);
   const float mf = a.mean[j * a.C + c], isf = a.istd[j * a.C + c];
+  const float ga = a.gamma[(int64_t)j * a.pstride + c];
+  const float be = a.gamma[(int64_t)j * a.pstride + a.C + c];
   const int64_t base = ((int64_t)j * a.b * a.C + c) * HW;
   double s = 0.0, sx = 0.0;
   ChanIter it(e0 + threadIdx.x, HW);
@@ -143,6 +145,7 @@ __global__ __launch_bounds__(256) void bn_bwd_stats_k(BNBwdArgs a) {
     const int64_t off = base + (int64_t)it.img * a.C * HW + it.p;
     float d = a.dy[off];
     if (a.y && !(a.y[off] > 0.f)) d = 0.f;
+    if (!a.y && a.relu_x && !(bn_affine(a.x[off], mf, isf, ga, be) > 0.f)) d = 0.f;
     const float xh = (a.x[off] - mf) * isf;
     s += d;
     sx += (double)d * xh;
@@ -170,6 +173,7 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BNBwdArgs a) {
   block_sum2(s, sx, red);
   const float mf = a.mean[j * a.C + c], isf = a.istd[j * a.C + c];
   const float ga = a.gamma[(int64_t)j * a.pstride + c];
+  const float be = a.gamma[(int64_t)j * a.pstride + a.C + c];
   if (chunk == 0 && threadIdx.x == 0) {
     a.dgamma[(int64_t)j * a.pstride + c] = (float)sx;
     a.dgamma[(int64_t)j * a.pstride + a.C + c] = (float)s;
@@ -181,6 +185,7 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_k(BNBwdArgs a) {
     const int64_t off = base + (int64_t)it.img * a.C * HW + it.p;
     float d = a.dy[off];
     if (a.y && !(a.y[off] > 0.f)) d = 0.f;
+    if (!a.y && a.relu_x && !(bn_affine(a.x[off], mf, isf, ga, be) > 0.f)) d = 0.f;
     const float xh = (a.x[off] - mf) * isf;
     a.dx[off] = k1 * (d - mdy - xh * mdyx);
     if (a.dres) a.dres[off] = d;
@@ -268,7 +273,7 @@ __global__ __launch_bounds__(256) void bn_apply_v4_k(BNArgs a) {
       if (!qd[u].ok) continue;
       v4f v;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = ga * ((xv[u][i] - mf) * isf) + be;
+      for (int i = 0; i < 4; ++i) v[i] = bn_affine(xv[u][i], mf, isf, ga, be);
       if (a.res_mode == RES_SAME) {
         v += rv[u];
       } else if (a.res_mode == RES_SUBSAMPLE && c < a.res_C) {
@@ -325,6 +330,7 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_v4_k(BNBwdArgs a) {
   const int n = a.b * HW;
   const float mf = a.mean[j * a.C + c], isf = a.istd[j * a.C + c];
   const float ga = a.gamma[(int64_t)j * a.pstride + c];
+  const float be = a.gamma[(int64_t)j * a.pstride + a.C + c];
   if (chunk == 0 && threadIdx.x == 0) {
     a.dgamma[(int64_t)j * a.pstride + c] = (float)sx;
     a.dgamma[(int64_t)j * a.pstride + a.C + c] = (float)s;
@@ -335,10 +341,15 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_v4_k(BNBwdArgs a) {
     for (int u = 0; u < BN_U; ++u) {
       if (!qd[u].ok) continue;
       v4f d = dv[u], dx;
-      if (a.y)
+      if (a.y) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           if (!(yv[u][i] > 0.f)) d[i] = 0.f;
+      } else if (a.relu_x) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (!(bn_affine(xv[u][i], mf, isf, ga, be) > 0.f)) d[i] = 0.f;
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float xh = (xv[u][i] - mf) * isf;

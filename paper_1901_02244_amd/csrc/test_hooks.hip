@@ -118,10 +118,12 @@ int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int st
                        const float* dy, const float* params, int64_t pstride, float* dx,
                        int accumulate, const float* mask, const float* add, int add_mode,
                        int add_C, const float* bn_x, const float* bn_y, const float* bn_mean,
-                       const float* bn_istd, double* bn_part, void* stream) {
+                       const float* bn_istd, const float* bn_gamma, double* bn_part,
+                       void* stream) {
   if (!geom_ok(k, b, Ci, H, W, Co, R, stride, pad) || !conv_supported(R, R, stride, true) ||
       !dy || !params || !dx || add_mode < ADD_NONE || add_mode > ADD_SUBSAMPLE ||
-      (add_mode != ADD_NONE && !add) || (bn_part && (!bn_x || !bn_mean || !bn_istd)))
+      (add_mode != ADD_NONE && !add) || (bn_part && (!bn_x || !bn_mean || !bn_istd)) ||
+      (bn_gamma && !bn_y))
     return CB_EINVAL;
   ConvBwdDataArgs d;
   d.g = make_geom(k, b, Ci, H, W, Co, R, stride, pad);
@@ -140,6 +142,7 @@ int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int st
   d.bn_y = bn_y;
   d.bn_mean = bn_mean;
   d.bn_istd = bn_istd;
+  d.bn_gamma = bn_gamma;
   return rc_of(conv_bwd_data(d, static_cast<hipStream_t>(stream)));
 }
 
@@ -175,11 +178,11 @@ int cb_test_bn_fwd(int k, int b, int C, int H, int W, int relu, const float* x,
 }
 
 int cb_test_bn_bwd(int k, int b, int C, int H, int W, const float* x, const float* mask_y,
-                   const float* dy, const float* params, int64_t pstride, const float* mean,
-                   const float* istd, float* dx, float* grads, void* scratch,
+                   int relu_x, const float* dy, const float* params, int64_t pstride,
+                   const float* mean, const float* istd, float* dx, float* grads, void* scratch,
                    size_t scratch_bytes, void* stream) {
   if (k < 1 || b < 1 || C < 1 || H < 1 || W < 1 || !x || !dy || !params || !mean || !istd ||
-      !dx || !grads)
+      !dx || !grads || (mask_y && relu_x))
     return CB_EINVAL;
   if (scratch_bytes < cb_test_bn_scratch_bytes(k, b, C, H, W)) return CB_ENOMEM;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -187,6 +190,7 @@ int cb_test_bn_bwd(int k, int b, int C, int H, int W, const float* x, const floa
   a.k = k; a.b = b; a.C = C; a.H = H; a.W = W;
   a.x = x;
   a.y = mask_y;
+  a.relu_x = relu_x != 0;
   a.dy = dy;
   a.dx = dx;
   a.dres = nullptr;

@@ -205,7 +205,7 @@ def test_batchnorm_kernels(case):
     mask = _dev(yo.astype(np.float32)) if relu else None
     dxd = torch.empty_like(xd)
     gd = torch.zeros_like(pd)
-    assert L.cb_test_bn_bwd(k, b, C, H, W, xd.data_ptr(), mask.data_ptr() if relu else None,
+    assert L.cb_test_bn_bwd(k, b, C, H, W, xd.data_ptr(), mask.data_ptr() if relu else None, 0,
                             dyd.data_ptr(), pd.data_ptr(), pstride, mean.data_ptr(),
                             istd.data_ptr(), dxd.data_ptr(), gd.data_ptr(), scratch.data_ptr(), sn,
                             st) == 0
@@ -220,6 +220,64 @@ def test_batchnorm_kernels(case):
     for j in range(k):
         _, dxo, dgo, dbo = ref[j]
         assert max_rel(dx[j * b:(j + 1) * b], dxo) <= TOL_STEP1, (name, j, "dx")
+        assert max_rel(g[j * pstride:j * pstride + C], dgo) <= TOL_STEP1, (name, j, "dgamma")
+        assert max_rel(g[j * pstride + C:j * pstride + 2 * C], dbo) <= TOL_STEP1, (name, j, "dbeta")
+
+
+def _bn_relu_from_x(x, mean, istd, gam, bet):
+    """The norm's ReLU decision as the kernels take it: (x - mean) * istd in
+    fp32, then gamma * t + beta rounded once (a fused multiply-add; the
+    product of two fp32 values is exact in fp64), positive or not."""
+    t = (x - mean[None, :, None, None]) * istd[None, :, None, None]
+    v = gam[None, :, None, None].astype(np.float64) * t.astype(np.float64) + \
+        bet[None, :, None, None].astype(np.float64)
+    return v > 0
+
+
+@pytest.mark.parametrize("case", [c for c in BN if c[-1]], ids=[c[0] for c in BN if c[-1]])
+def test_batchnorm_backward_relu_mask_from_x(case):
+    """A norm with a ReLU and no residual input: the backward recomputes the
+    ReLU decision from x and takes exactly the forward's (checked bitwise
+    against the forward's output), and its gradients match the oracle's
+    given that decision."""
+    name, k, b, C, H, _ = case
+    W = H
+    rng = _rng("bnx" + name)
+    x = (rng.standard_normal((k * b, C, H, W), dtype=np.float32) * 2 + 0.5).astype(np.float32)
+    dy = rng.standard_normal((k * b, C, H, W), dtype=np.float32)
+    pstride = 2 * C + 1
+    params = np.zeros(k * pstride, dtype=np.float32)
+    for j in range(k):
+        params[j * pstride:j * pstride + C] = 1 + 0.2 * rng.standard_normal(C)
+        params[j * pstride + C:j * pstride + 2 * C] = 0.2 * rng.standard_normal(C)
+    L = cb.lib()
+    sn = L.cb_test_bn_scratch_bytes(k, b, C, H, W)
+    xd, dyd, pd = _dev(x), _dev(dy), _dev(params)
+    yd = torch.empty_like(xd)
+    mean = torch.empty(k * C, dtype=torch.float32, device="cuda")
+    istd = torch.empty(k * C, dtype=torch.float32, device="cuda")
+    scratch = torch.empty(sn, dtype=torch.uint8, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    assert L.cb_test_bn_fwd(k, b, C, H, W, 1, xd.data_ptr(), pd.data_ptr(), pstride,
+                            yd.data_ptr(), mean.data_ptr(), istd.data_ptr(), scratch.data_ptr(),
+                            sn, st) == 0
+    dxd = torch.empty_like(xd)
+    gd = torch.zeros_like(pd)
+    assert L.cb_test_bn_bwd(k, b, C, H, W, xd.data_ptr(), None, 1, dyd.data_ptr(), pd.data_ptr(),
+                            pstride, mean.data_ptr(), istd.data_ptr(), dxd.data_ptr(),
+                            gd.data_ptr(), scratch.data_ptr(), sn, st) == 0
+    torch.cuda.synchronize()
+    y = yd.cpu().numpy()
+    mf, isf = mean.cpu().numpy().reshape(k, C), istd.cpu().numpy().reshape(k, C)
+    dx, g = dxd.cpu().numpy(), gd.cpu().numpy()
+    for j in range(k):
+        sl = slice(j * b, (j + 1) * b)
+        gam = params[j * pstride:j * pstride + C]
+        bet = params[j * pstride + C:j * pstride + 2 * C]
+        on = _bn_relu_from_x(x[sl], mf[j], isf[j], gam, bet)
+        np.testing.assert_array_equal(on, y[sl] > 0, err_msg=f"{name} replica {j}")
+        _, dxo, dgo, dbo = oracle.batchnorm(x[sl], gam, bet, dy=np.where(on, dy[sl], 0.0))
+        assert max_rel(dx[sl], dxo) <= TOL_STEP1, (name, j, "dx")
         assert max_rel(g[j * pstride:j * pstride + C], dgo) <= TOL_STEP1, (name, j, "dgamma")
         assert max_rel(g[j * pstride + C:j * pstride + 2 * C], dbo) <= TOL_STEP1, (name, j, "dbeta")
 
@@ -284,7 +342,8 @@ def test_softmax_xent_kernel(case):
         assert max_rel(d[j * b:(j + 1) * b], do) <= TOL_STEP1
 
 
-# (name, k, b, Ci, H, Co, R, stride, pad, accumulate, mask, add_mode, add_C, bn, bn_y)
+# (name, k, b, Ci, H, Co, R, stride, pad, accumulate, mask, add_mode, add_C, bn, bn_y:
+#  0 none, 1 a y tensor, 2 a y tensor that gamma and beta recompute from bn_x)
 DGRAD_EPILOGUE = [
     ("direct.w32.same.bn", 2, 4, 16, 32, 16, 3, 1, 1, 1, 1, 1, 16, 1, 1),
     ("direct.w16.bn", 2, 3, 32, 16, 32, 3, 1, 1, 0, 0, 0, 0, 1, 1),
@@ -297,6 +356,13 @@ DGRAD_EPILOGUE = [
     # 1x1 stride 2 on even planes: the GEMM over the output grid only
     ("gemm.1x1s2.grid.acc.mask.same.bn", 2, 3, 24, 14, 40, 1, 2, 0, 1, 1, 1, 24, 1, 1),
     ("gemm.1x1s2.grid.sub.bn", 2, 5, 20, 10, 36, 1, 2, 0, 0, 0, 2, 20, 1, 0),
+    # bn_y = 2: the norm's ReLU output recomputed from bn_x (a norm with no residual input)
+    ("direct.w32.same.bn.relux", 2, 4, 16, 32, 16, 3, 1, 1, 1, 0, 1, 16, 1, 2),
+    ("direct.w8.bn.relux", 2, 3, 64, 8, 64, 3, 1, 1, 0, 0, 0, 0, 1, 2),
+    ("s2.w16.sub.bn.relux", 2, 4, 32, 16, 64, 3, 2, 1, 0, 0, 2, 64, 1, 2),
+    ("gemm.3x3s2.ragged.bn.relux", 2, 3, 7, 13, 19, 3, 2, 1, 0, 0, 0, 0, 1, 2),
+    ("gemm.5x5.bn.relux", 2, 4, 6, 14, 16, 5, 1, 0, 0, 0, 0, 0, 1, 2),
+    ("gemm.1x1s2.grid.acc.same.bn.relux", 2, 3, 24, 14, 40, 1, 2, 0, 1, 0, 1, 24, 1, 2),
 ]
 
 
@@ -324,21 +390,34 @@ def test_conv_data_gradient_epilogue(case):
     elif add_mode == 2:
         add = rng.standard_normal((N, add_C, Ho, Ho), dtype=np.float32)
     bn_x = rng.standard_normal((N, Ci, H, H), dtype=np.float32) if bn else None
-    bn_y = rng.standard_normal((N, Ci, H, H), dtype=np.float32) if (bn and use_y) else None
+    bn_y = rng.standard_normal((N, Ci, H, H), dtype=np.float32) if (bn and use_y == 1) else None
     mean = (rng.standard_normal((k, Ci)) * 0.1).astype(np.float32) if bn else None
     istd = (rng.uniform(0.5, 2.0, (k, Ci))).astype(np.float32) if bn else None
+    # use_y == 2: gamma and beta are given too, and bn_y is the sign of the
+    # norm's output recomputed from bn_x, so reading it and recomputing it
+    # must give the same mask
+    gb = np.zeros(k * pstride, dtype=np.float32)
+    for j in range(k):
+        gb[j * pstride:j * pstride + Ci] = 1 + 0.3 * rng.standard_normal(Ci)
+        gb[j * pstride + Ci:j * pstride + 2 * Ci] = 0.5 * rng.standard_normal(Ci)
+    if bn and use_y == 2:
+        bn_y = np.concatenate([np.where(
+            _bn_relu_from_x(bn_x[j * b:(j + 1) * b], mean[j], istd[j],
+                            gb[j * pstride:j * pstride + Ci],
+                            gb[j * pstride + Ci:j * pstride + 2 * Ci]), 1.0, -1.0)
+            for j in range(k)]).astype(np.float32)
     L = cb.lib()
     parts = L.cb_test_conv_dgrad_parts(k, b, Ci, H, H, Co, R, st, pad)
     assert parts > 0
     d = {n_: (_dev(v) if v is not None else None) for n_, v in
          dict(dy=dy, p=params, dx=dx0, mask=mask, add=add, x=bn_x, y=bn_y, mean=mean,
-              istd=istd).items()}
+              istd=istd, g=gb if (bn and use_y == 2) else None).items()}
     part = torch.zeros(k * Ci * parts * 2, dtype=torch.float64, device="cuda") if bn else None
     ptr = lambda t: t.data_ptr() if t is not None else None
     rc = L.cb_test_conv_dgrad(k, b, Ci, H, H, Co, R, st, pad, ptr(d["dy"]), ptr(d["p"]), pstride,
                               ptr(d["dx"]), acc, ptr(d["mask"]), ptr(d["add"]), add_mode, add_C,
                               ptr(d["x"]), ptr(d["y"]), ptr(d["mean"]), ptr(d["istd"]),
-                              ptr(part), torch.cuda.current_stream().cuda_stream)
+                              ptr(d["g"]), ptr(part), torch.cuda.current_stream().cuda_stream)
     assert rc == 0
     torch.cuda.synchronize()
     got = d["dx"].cpu().numpy()
