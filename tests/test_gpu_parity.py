@@ -573,6 +573,33 @@ def test_graph_replay_is_bitwise_direct():
     graph.close()
 
 
+def test_graph_cache_eviction_is_bitwise_direct():
+    """More (inputs, labels) pairs than graphs kept: the oldest graphs are
+    dropped and recaptured, and every step still matches direct launches
+    bitwise."""
+    m = cb.model("lenet5", 1, 28, 28, 10)
+    w0 = wl.init_w0(cb.cb_tensor_layout(m), 12)
+    k, b = 3, 4
+    direct = cb.Context(m, k, b, 1.0 / 3, 0.01, 0.9, w0)
+    graph = cb.Context(m, k, b, 1.0 / 3, 0.01, 0.9, w0)
+    graph.cb_set_graphs(True)
+    ring = [tuple(_dev(a) for a in wl.batch(k * b, 1, 28, 28, 10, 12, t)) for t in range(10)]
+    for it in range(25):
+        x, y = ring[(it * 3) % 10]
+        for ctx in (direct, graph):
+            ctx.cb_step(x, y)
+            ctx.cb_sync()
+        np.testing.assert_array_equal(direct.cb_get_central(), graph.cb_get_central(),
+                                      err_msg=f"iteration {it}")
+    graph.cb_set_graphs(False)  # back to direct launches
+    for ctx in (direct, graph):
+        ctx.cb_step(*ring[0])
+        ctx.cb_sync()
+    np.testing.assert_array_equal(direct.cb_get_central(), graph.cb_get_central())
+    direct.close()
+    graph.close()
+
+
 # ------------------------------------------------------------ error paths
 
 def test_error_paths():
