@@ -58,6 +58,10 @@ struct Op {
   bool dx_accumulate = false, dx_mask = false;
   int add_mode = ADD_NONE, add_C = 0, add_st = 1;
   int64_t add_buf = -1;
+  // fused head: a pool, FC and softmax cross-entropy run as one kernel
+  // (launched at the pool; the FC keeps its weight gradient)
+  bool head = false;
+  int head_fc = -1, head_bn = -1;   // at the pool: the FC op, the batch norm feeding the pool
 };
 
 struct ParamInfo {
@@ -74,6 +78,7 @@ struct Plan {
   std::vector<ParamInfo> params;
   int64_t P = 0, Pp = 0;
   int input = -1, logits = -1;
+  bool loss_per_image = false;  // the loss buffer holds k*b per-image terms (fused head)
   // workspace layout (bytes)
   int64_t off_W = 0, off_G = 0, off_Z = 0, off_Zp = 0, off_Wprev = -1;
   int64_t off_loss = 0, off_flag = 0, off_bnpart = 0;
@@ -380,6 +385,30 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p, int kcap = 0) {
       }
     }
   }
+  // The head -- global average pool, an FC layer with few classes and no
+  // ReLU, softmax cross-entropy -- runs as one kernel per image, which also
+  // writes the backward sums of the batch norm feeding the pool (one part
+  // per image).
+  for (size_t i = 0; i + 2 < p.ops.size(); ++i) {
+    Op& gp = p.ops[i];
+    Op& fc = p.ops[i + 1];
+    Op& xe = p.ops[i + 2];
+    if (gp.kind != OP_GAP || fc.kind != OP_CONV || xe.kind != OP_XENT) continue;
+    if (fc.in != gp.out || xe.in != fc.out || fc.R != 1 || fc.H != 1 || fc.W != 1 || fc.relu ||
+        !fc.need_dx || !head_ok(gp.C, gp.H * gp.W, fc.Co) ||
+        p.t[gp.out].consumers != 1 || p.t[fc.out].consumers != 1)
+      continue;
+    gp.head = fc.head = xe.head = true;
+    gp.head_fc = (int)i + 1;
+    p.loss_per_image = true;
+    if (i > 0) {
+      Op& bn = p.ops[i - 1];
+      if (bn.kind == OP_BN && bn.out == gp.in && p.t[gp.in].consumers == 1 && bn.bwd_parts == 0) {
+        bn.bwd_parts = b;
+        gp.head_bn = (int)i - 1;
+      }
+    }
+  }
   int64_t bnpart = 0;
   for (size_t i = 0; i < p.ops.size(); ++i) {
     Op& o = p.ops[i];
@@ -408,7 +437,7 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p, int kcap = 0) {
   for (Op& o : p.ops)
     if (o.kind == OP_CONV && o.add_mode != ADD_NONE) o.add_buf = p.ops[o.add_buf].dres;
   p.off_bnpart = take(std::max<int64_t>(bnpart, 16));
-  p.off_loss = take((int64_t)k * 4);
+  p.off_loss = take((int64_t)k * b * 4);
   p.off_flag = take(16);
   p.total = off;
   return true;
@@ -584,9 +613,11 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
   float* G = c->G();
 
   // forward, all learners in every launch
-  for (const Op& o : p.ops) {
+  for (size_t oi = 0; oi < p.ops.size(); ++oi) {
+    const Op& o = p.ops[oi];
     switch (o.kind) {
       case OP_CONV: {
+        if (o.head) break;  // inside the fused head
         ConvFwdArgs a;
         a.g = geom(p, o);
         a.x = act(o.in);
@@ -637,11 +668,45 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
                   maxpool_fwd(act(o.in), N, o.C, o.H, o.W, o.K, o.st, o.pad, act(o.out), o.Ho,
                               o.Wo, c->at<int>(o.arg), s));
         break;
-      case OP_GAP:
-        CB_LAUNCH(c, "gap_fwd_k", 0.0, 4.0 * N * o.C * (o.H * o.W + 1.0),
-                  gap_fwd(act(o.in), N, o.C, o.H * o.W, act(o.out), s));
+      case OP_GAP: {
+        if (!o.head) {
+          CB_LAUNCH(c, "gap_fwd_k", 0.0, 4.0 * N * o.C * (o.H * o.W + 1.0),
+                    gap_fwd(act(o.in), N, o.C, o.H * o.W, act(o.out), s));
+          break;
+        }
+        const Op& fc = p.ops[o.head_fc];
+        HeadArgs a;
+        a.k = k; a.b = b; a.C = o.C; a.HW = o.H * o.W; a.classes = fc.Co;
+        a.y = act(o.in);
+        a.g = act(o.out);
+        a.w = W + fc.w_off;
+        a.bias = fc.bias ? W + fc.b_off : nullptr;
+        a.pstride = p.Pp;
+        a.labels = labels;
+        a.dlogits = grd(fc.out);
+        a.loss = c->at<float>(p.off_loss);
+        a.dy = grd(o.in);
+        a.bn_part = nullptr;
+        a.bn_relu = 0;
+        a.bn_x = a.bn_mean = a.bn_istd = nullptr;
+        if (o.head_bn >= 0) {
+          const Op& bn = p.ops[o.head_bn];
+          a.bn_part = c->at<double>(p.off_bnpart);
+          a.bn_relu = bn.relu;
+          a.bn_x = act(bn.in);
+          a.bn_mean = c->at<float>(bn.mean);
+          a.bn_istd = c->at<float>(bn.istd);
+        }
+        // the pooled tensor (read twice), its gradient, the norm's x, the
+        // FC weights, features, logit gradients
+        const double plane = (double)N * o.C * o.H * o.W;
+        const double bytes = 4.0 * (plane * (2.0 + (o.head_bn >= 0 ? 1.0 : 0.0)) +
+                                    (double)k * fc.Co * o.C + (double)N * (o.C + 2.0 * fc.Co + 2.0));
+        CB_LAUNCH(c, "head_k", 0.0, bytes, head_fwd_bwd(a, s));
         break;
+      }
       case OP_XENT:
+        if (o.head) break;  // inside the fused head
         CB_LAUNCH(c, "softmax_xent_k", 0.0, 4.0 * N * (2.0 * p.m.num_classes + 1),
                   softmax_xent(act(o.in), labels, k, b, p.m.num_classes, grd(o.in),
                                c->at<float>(p.off_loss), s, &nm_));
@@ -654,6 +719,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
     switch (o.kind) {
       case OP_XENT: break;
       case OP_GAP:
+        if (o.head) break;  // done by the fused head
         CB_LAUNCH(c, "gap_bwd_k", 0.0, 4.0 * N * o.C * (o.H * o.W + 1.0),
                   gap_bwd(grd(o.out), N, o.C, o.H * o.W, grd(o.in), s, &nm_));
         break;
@@ -722,7 +788,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
           CB_HIP(c, conv_bwd_weight(w, ss, &nm));
           ps.done(nm, flops, 4.0 * (xin + yout + k * wn));
         }
-        if (o.need_dx) {
+        if (o.need_dx && !o.head) {  // a head FC's dx comes from the fused head
           ConvBwdDataArgs d;
           d.g = g;
           d.dy = grd(o.out);
@@ -1061,7 +1127,20 @@ int cb_get_grad(cb_ctx* c, int j, float* out_host, int64_t n) {
 
 int cb_get_loss(cb_ctx* c, float* out_host) {
   if (!c) return CB_EINVAL;
-  return copy_out(c, c->at<float>(c->p.off_loss), out_host, c->p.k, c->p.k);
+  const Plan& p = c->p;
+  if (!p.loss_per_image) return copy_out(c, c->at<float>(p.off_loss), out_host, p.k, p.k);
+  // per-image terms: each replica's mean in image order, in fp64
+  if (!out_host) return fail(c, CB_EINVAL, "output is NULL");
+  std::vector<float> terms((size_t)p.k * p.b);
+  const int rc = copy_out(c, c->at<float>(p.off_loss), terms.data(), (int64_t)terms.size(),
+                          (int64_t)terms.size());
+  if (rc) return rc;
+  for (int j = 0; j < p.k; ++j) {
+    double t = 0.0;
+    for (int n = 0; n < p.b; ++n) t += (double)terms[(size_t)j * p.b + n];
+    out_host[j] = (float)(t / p.b);
+  }
+  return CB_OK;
 }
 
 int cb_sma_apply(cb_ctx* c, const float* grads_dev) {

@@ -228,6 +228,34 @@ hipError_t gap_fwd(const float* x, int N, int C, int HW, float* y, hipStream_t s
 hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t s,
                    const char** name = nullptr);
 // Mean softmax cross-entropy per replica and its gradient wrt the logits.
+// The network head of one image in one launch: global average pool, an FC
+// layer with at most HEAD_MAX_CLASSES outputs (no ReLU), softmax
+// cross-entropy, then the backward down to the pooled tensor's gradient
+// (and the backward partial sums of the batch norm that produced it).
+constexpr int HEAD_MAX_C = 1024, HEAD_MAX_CLASSES = 32;
+struct HeadArgs {
+  int k, b, C, HW, classes;
+  const float* y;        // pooled input [k*b][C][HW]
+  float* g;              // pooled features [k*b][C] (the FC input, kept for its weight gradient)
+  const float* w;        // replica 0 FC weights [classes][C]
+  const float* bias;     // replica 0 bias [classes], or nullptr
+  int64_t pstride;
+  const int32_t* labels; // [k*b]
+  float* dlogits;        // [k*b][classes]
+  float* loss;           // per image [k*b]; a replica's loss is the mean of its b
+  float* dy;             // gradient at the pooled input [k*b][C][HW]
+  // If bn_part is set, y is the output of a batch norm (ReLU'd if bn_relu):
+  // its backward partial sums per image as in ConvBwdDataArgs, [k][C][b][2].
+  double* bn_part;
+  int bn_relu;
+  const float* bn_x;
+  const float* bn_mean;
+  const float* bn_istd;
+};
+// Shapes the head kernel takes: C <= HEAD_MAX_C, 1 <= classes <=
+// HEAD_MAX_CLASSES, HW a multiple of 4 with HW/4 a power of two up to 64.
+bool head_ok(int C, int HW, int classes);
+hipError_t head_fwd_bwd(const HeadArgs& a, hipStream_t s);
 hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b, int classes,
                         float* dlogits, float* loss, hipStream_t s,
                         const char** name = nullptr);

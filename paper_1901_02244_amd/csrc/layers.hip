@@ -16,6 +16,7 @@ namespace {
 constexpr double BN_EPS = 1e-5;
 
 inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+inline bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 __device__ __forceinline__ double wave_sum_d(double v) {
 #pragma unroll
@@ -513,7 +514,110 @@ __global__ __launch_bounds__(256) void softmax_xent_rows_k(const float* logits,
   if (threadIdx.x == 0) loss[j] = (float)((((red[0] + red[1]) + red[2]) + red[3]) / b);
 }
 
+// The head of one image, block (n, j).  A channel's HW pixels are HW/4
+// float4s, one per thread of a group of TPC = HW/4 lanes (a power of two up
+// to 64), so a pass covers 256/TPC channels with every load in flight, and
+// a channel's sums combine by xor butterfly within its group.  Logits: a
+// wave per class, lanes over channels.  Softmax cross-entropy: wave 0, a
+// lane per class (the same arithmetic per row as softmax_xent_rows_k).
+// Features' gradient: a thread per channel, in class order.  Then the pool
+// backward with the batch norm's partial sums (fp64).
+__device__ __forceinline__ float group_sum_f(float v, int tpc) {
+  for (int o = 1; o < tpc; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double group_sum_d(double v, int tpc) {
+  for (int o = 1; o < tpc; o <<= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void head_k(HeadArgs a) {
+  __shared__ float gs[HEAD_MAX_C], dgs[HEAD_MAX_C], ls[HEAD_MAX_CLASSES];
+  const int n = blockIdx.x, j = blockIdx.y, row = j * a.b + n;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int tpc = a.HW >> 2, cpp = 256 / tpc;  // threads per channel, channels per pass
+  const int cg = threadIdx.x / tpc, q = threadIdx.x - cg * tpc;
+  const int64_t plane0 = (int64_t)row * a.C * a.HW;
+  const float* Y = a.y + plane0;
+  for (int c = cg; c < a.C; c += cpp) {
+    const v4f v = *reinterpret_cast<const v4f*>(Y + (int64_t)c * a.HW + 4 * q);
+    const float s = group_sum_f(((v[0] + v[1]) + v[2]) + v[3], tpc);
+    if (q == 0) {
+      gs[c] = s / a.HW;
+      a.g[(int64_t)row * a.C + c] = s / a.HW;
+    }
+  }
+  __syncthreads();
+  const float* Wf = a.w + (int64_t)j * a.pstride;
+  for (int o = w; o < a.classes; o += 4) {
+    float s = 0.f;
+    for (int c = lane; c < a.C; c += 64) s += Wf[(int64_t)o * a.C + c] * gs[c];
+    s = wave_sum_f(s);
+    if (lane == 0) ls[o] = a.bias ? s + a.bias[(int64_t)j * a.pstride + o] : s;
+  }
+  __syncthreads();
+  if (w == 0) {
+    const bool on = lane < a.classes;
+    const float o = on ? ls[lane] : -INFINITY;
+    const float mx = wave_max_f(o);
+    const float lse = mx + logf(wave_sum_f(on ? expf(o - mx) : 0.f));
+    const int y = a.labels[row];
+    const bool yok = (unsigned)y < (unsigned)a.classes;
+    if (lane == 0) a.loss[row] = yok ? lse - ls[y] : NAN;
+    __builtin_amdgcn_wave_barrier();
+    if (on) {
+      const float d = (expf(o - lse) - (lane == y ? 1.f : 0.f)) / a.b;
+      ls[lane] = d;
+      a.dlogits[(int64_t)row * a.classes + lane] = d;
+    }
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < a.C; c += 256) {
+    float s = 0.f;
+    for (int o = 0; o < a.classes; ++o) s += ls[o] * Wf[(int64_t)o * a.C + c];
+    dgs[c] = s;
+  }
+  __syncthreads();
+  float* DY = a.dy + plane0;
+  for (int c = cg; c < a.C; c += cpp) {
+    const float d0 = dgs[c] / a.HW;
+    const int64_t idx = (int64_t)c * a.HW + 4 * q;
+    *reinterpret_cast<v4f*>(DY + idx) = v4f{d0, d0, d0, d0};
+    if (!a.bn_part) continue;  // uniform: the whole block takes the same branch
+    const v4f yv = *reinterpret_cast<const v4f*>(Y + idx);
+    const v4f xv = *reinterpret_cast<const v4f*>(a.bn_x + plane0 + idx);
+    const float bm = a.bn_mean[j * a.C + c], bi = a.bn_istd[j * a.C + c];
+    double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float d = (!a.bn_relu || yv[i] > 0.f) ? d0 : 0.f;
+      s1 += (double)d;
+      s2 += (double)d * ((xv[i] - bm) * bi);
+    }
+    s1 = group_sum_d(s1, tpc);
+    s2 = group_sum_d(s2, tpc);
+    if (q == 0) {
+      double* pq = a.bn_part + (((int64_t)j * a.C + c) * a.b + n) * 2;
+      pq[0] = s1;
+      pq[1] = s2;
+    }
+  }
+}
+
 }  // namespace
+
+bool head_ok(int C, int HW, int classes) {
+  const int tpc = HW / 4;
+  return C <= HEAD_MAX_C && classes >= 1 && classes <= HEAD_MAX_CLASSES && HW % 4 == 0 &&
+         tpc >= 1 && tpc <= 64 && (tpc & (tpc - 1)) == 0;
+}
+
+hipError_t head_fwd_bwd(const HeadArgs& a, hipStream_t s) {
+  if (!head_ok(a.C, a.HW, a.classes) || !al16(a.y) || !al16(a.dy) || !al16(a.bn_x))
+    return hipErrorInvalidValue;
+  klaunch(head_k, dim3(a.b, a.k), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
 
 int bn_chunks(int b, int HW, int C, int k) {
   const int n = b * HW;
@@ -527,7 +631,6 @@ hipError_t bn_fwd_stats(const BNArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-inline bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 hipError_t bn_fwd_apply(const BNArgs& a, hipStream_t s, const char** name) {
   if ((a.H * a.W) % 4 == 0 && al16(a.x) && al16(a.y) && (a.res_mode != RES_SAME || al16(a.res))) {
