@@ -233,6 +233,9 @@ hipError_t gap_bwd(const float* dy, int N, int C, int HW, float* dx, hipStream_t
 // cross-entropy, then the backward down to the pooled tensor's gradient
 // (and the backward partial sums of the batch norm that produced it).
 constexpr int HEAD_MAX_C = 1024, HEAD_MAX_CLASSES = 32;
+// per image at most HEAD_MAX_PLANE pooled values (HEAD_PASSES float4s per
+// thread) and HEAD_MAX_W FC weights (staged in LDS)
+constexpr int HEAD_MAX_PLANE = 4096, HEAD_PASSES = HEAD_MAX_PLANE / 1024, HEAD_MAX_W = 4096;
 struct HeadArgs {
   int k, b, C, HW, classes;
   const float* y;        // pooled input [k*b][C][HW]
@@ -253,7 +256,8 @@ struct HeadArgs {
   const float* bn_istd;
 };
 // Shapes the head kernel takes: C <= HEAD_MAX_C, 1 <= classes <=
-// HEAD_MAX_CLASSES, HW a multiple of 4 with HW/4 a power of two up to 64.
+// HEAD_MAX_CLASSES, HW a multiple of 4 with HW/4 a power of two up to 64,
+// C*HW <= HEAD_MAX_PLANE, classes*C <= HEAD_MAX_W.
 bool head_ok(int C, int HW, int classes);
 hipError_t head_fwd_bwd(const HeadArgs& a, hipStream_t s);
 hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b, int classes,

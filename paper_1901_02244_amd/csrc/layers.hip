@@ -533,27 +533,52 @@ __device__ __forceinline__ double group_sum_d(double v, int tpc) {
 
 __global__ __launch_bounds__(256) void head_k(HeadArgs a) {
   __shared__ float gs[HEAD_MAX_C], dgs[HEAD_MAX_C], ls[HEAD_MAX_CLASSES];
+  __shared__ float wsh[HEAD_MAX_W], bsh[HEAD_MAX_CLASSES], msh[HEAD_MAX_C], ish[HEAD_MAX_C];
   const int n = blockIdx.x, j = blockIdx.y, row = j * a.b + n;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int tpc = a.HW >> 2, cpp = 256 / tpc;  // threads per channel, channels per pass
   const int cg = threadIdx.x / tpc, q = threadIdx.x - cg * tpc;
   const int64_t plane0 = (int64_t)row * a.C * a.HW;
   const float* Y = a.y + plane0;
-  for (int c = cg; c < a.C; c += cpp) {
-    const v4f v = *reinterpret_cast<const v4f*>(Y + (int64_t)c * a.HW + 4 * q);
-    const float s = group_sum_f(((v[0] + v[1]) + v[2]) + v[3], tpc);
+  // every global read goes out first: the pooled plane and the norm's x
+  // (at most HEAD_PASSES float4s per thread), the FC weights and bias, the
+  // norm's statistics, the label
+  v4f yv[HEAD_PASSES], xv[HEAD_PASSES];
+#pragma unroll
+  for (int r = 0; r < HEAD_PASSES; ++r) {
+    const int c = cg + r * cpp;
+    if (c < a.C) {
+      const int64_t idx = (int64_t)c * a.HW + 4 * q;
+      yv[r] = *reinterpret_cast<const v4f*>(Y + idx);
+      if (a.bn_part) xv[r] = *reinterpret_cast<const v4f*>(a.bn_x + plane0 + idx);
+    }
+  }
+  const float* Wf = a.w + (int64_t)j * a.pstride;
+  for (int e = threadIdx.x; e < a.classes * a.C; e += 256) wsh[e] = Wf[e];
+  if ((int)threadIdx.x < a.classes)
+    bsh[threadIdx.x] = a.bias ? a.bias[(int64_t)j * a.pstride + threadIdx.x] : 0.f;
+  if (a.bn_part)
+    for (int c = threadIdx.x; c < a.C; c += 256) {
+      msh[c] = a.bn_mean[j * a.C + c];
+      ish[c] = a.bn_istd[j * a.C + c];
+    }
+  const int label = a.labels[row];
+#pragma unroll
+  for (int r = 0; r < HEAD_PASSES; ++r) {
+    const int c = cg + r * cpp;
+    if (c >= a.C) continue;  // whole channel groups, so group_sum stays within active lanes
+    const float s = group_sum_f(((yv[r][0] + yv[r][1]) + yv[r][2]) + yv[r][3], tpc);
     if (q == 0) {
       gs[c] = s / a.HW;
       a.g[(int64_t)row * a.C + c] = s / a.HW;
     }
   }
   __syncthreads();
-  const float* Wf = a.w + (int64_t)j * a.pstride;
   for (int o = w; o < a.classes; o += 4) {
     float s = 0.f;
-    for (int c = lane; c < a.C; c += 64) s += Wf[(int64_t)o * a.C + c] * gs[c];
+    for (int c = lane; c < a.C; c += 64) s += wsh[o * a.C + c] * gs[c];
     s = wave_sum_f(s);
-    if (lane == 0) ls[o] = a.bias ? s + a.bias[(int64_t)j * a.pstride + o] : s;
+    if (lane == 0) ls[o] = a.bias ? s + bsh[o] : s;
   }
   __syncthreads();
   if (w == 0) {
@@ -561,12 +586,11 @@ __global__ __launch_bounds__(256) void head_k(HeadArgs a) {
     const float o = on ? ls[lane] : -INFINITY;
     const float mx = wave_max_f(o);
     const float lse = mx + logf(wave_sum_f(on ? expf(o - mx) : 0.f));
-    const int y = a.labels[row];
-    const bool yok = (unsigned)y < (unsigned)a.classes;
-    if (lane == 0) a.loss[row] = yok ? lse - ls[y] : NAN;
+    const bool yok = (unsigned)label < (unsigned)a.classes;
+    if (lane == 0) a.loss[row] = yok ? lse - ls[label] : NAN;
     __builtin_amdgcn_wave_barrier();
     if (on) {
-      const float d = (expf(o - lse) - (lane == y ? 1.f : 0.f)) / a.b;
+      const float d = (expf(o - lse) - (lane == label ? 1.f : 0.f)) / a.b;
       ls[lane] = d;
       a.dlogits[(int64_t)row * a.classes + lane] = d;
     }
@@ -574,25 +598,25 @@ __global__ __launch_bounds__(256) void head_k(HeadArgs a) {
   __syncthreads();
   for (int c = threadIdx.x; c < a.C; c += 256) {
     float s = 0.f;
-    for (int o = 0; o < a.classes; ++o) s += ls[o] * Wf[(int64_t)o * a.C + c];
+    for (int o = 0; o < a.classes; ++o) s += ls[o] * wsh[o * a.C + c];
     dgs[c] = s;
   }
   __syncthreads();
   float* DY = a.dy + plane0;
-  for (int c = cg; c < a.C; c += cpp) {
+#pragma unroll
+  for (int r = 0; r < HEAD_PASSES; ++r) {
+    const int c = cg + r * cpp;
+    if (c >= a.C) continue;
     const float d0 = dgs[c] / a.HW;
-    const int64_t idx = (int64_t)c * a.HW + 4 * q;
-    *reinterpret_cast<v4f*>(DY + idx) = v4f{d0, d0, d0, d0};
-    if (!a.bn_part) continue;  // uniform: the whole block takes the same branch
-    const v4f yv = *reinterpret_cast<const v4f*>(Y + idx);
-    const v4f xv = *reinterpret_cast<const v4f*>(a.bn_x + plane0 + idx);
-    const float bm = a.bn_mean[j * a.C + c], bi = a.bn_istd[j * a.C + c];
+    *reinterpret_cast<v4f*>(DY + (int64_t)c * a.HW + 4 * q) = v4f{d0, d0, d0, d0};
+    if (!a.bn_part) continue;  // uniform
+    const float bm = msh[c], bi = ish[c];
     double s1 = 0.0, s2 = 0.0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float d = (!a.bn_relu || yv[i] > 0.f) ? d0 : 0.f;
+      const float d = (!a.bn_relu || yv[r][i] > 0.f) ? d0 : 0.f;
       s1 += (double)d;
-      s2 += (double)d * ((xv[i] - bm) * bi);
+      s2 += (double)d * ((xv[r][i] - bm) * bi);
     }
     s1 = group_sum_d(s1, tpc);
     s2 = group_sum_d(s2, tpc);
@@ -609,7 +633,8 @@ __global__ __launch_bounds__(256) void head_k(HeadArgs a) {
 bool head_ok(int C, int HW, int classes) {
   const int tpc = HW / 4;
   return C <= HEAD_MAX_C && classes >= 1 && classes <= HEAD_MAX_CLASSES && HW % 4 == 0 &&
-         tpc >= 1 && tpc <= 64 && (tpc & (tpc - 1)) == 0;
+         tpc >= 1 && tpc <= 64 && (tpc & (tpc - 1)) == 0 && (int64_t)C * HW <= HEAD_MAX_PLANE &&
+         classes * C <= HEAD_MAX_W;
 }
 
 hipError_t head_fwd_bwd(const HeadArgs& a, hipStream_t s) {
