@@ -702,7 +702,9 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
         const double plane = (double)N * o.C * o.H * o.W;
         const double bytes = 4.0 * (plane * (2.0 + (o.head_bn >= 0 ? 1.0 : 0.0)) +
                                     (double)k * fc.Co * o.C + (double)N * (o.C + 2.0 * fc.Co + 2.0));
-        CB_LAUNCH(c, "head_k", 0.0, bytes, head_fwd_bwd(a, s));
+        // the FC's forward and data-gradient contractions
+        const double flops = 4.0 * N * o.C * fc.Co;
+        CB_LAUNCH(c, "head_k", flops, bytes, head_fwd_bwd(a, s));
         break;
       }
       case OP_XENT:
