@@ -822,7 +822,9 @@ int pick_tile(int64_t M, int N, int k) {
   auto wgs = [&](int bm, int bn) { return (int64_t)cdiv(M, bm) * cdiv(N, bn) * k; };
   if (N <= 16) return wgs(256, 16) >= MIN_WGS ? 0 : 1;
   if (N <= 32) return wgs(128, 32) >= MIN_WGS ? 2 : 3;
-  return wgs(128, 64) >= MIN_WGS ? 4 : 5;
+  if (wgs(128, 64) >= MIN_WGS) return 4;
+  // under one workgroup per CU even at 64 x 64: 16-column tiles (same rows)
+  return wgs(64, 64) >= MIN_WGS / 2 ? 5 : 1;
 }
 
 int tile_rows(int t) {
