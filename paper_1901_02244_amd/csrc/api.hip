@@ -457,6 +457,13 @@ struct ProfAgg {
   double ms = 0, flops = 0, bytes = 0;
 };
 
+// Weight gradients go to the side stream FORK_GROUP layers at a time behind
+// one fork event: each fork is an event record on the caller's stream and a
+// barrier packet on the side stream (ResNet-32, k=4, b=32: one fork per
+// layer 90.3k images/s, per two layers 93.1k, per three 93.2k, per four
+// 92.5k).
+constexpr int FORK_GROUP = 2;
+
 struct cb_ctx {
   Plan p;
   char* ws = nullptr;
@@ -477,9 +484,11 @@ struct cb_ctx {
   std::vector<int> split_after;  // per table: the operator whose weight gradient completes it
   bool split_per_layer = false;   // one table per layer
   int first_conv = -1;            // the first conv operator (the backward pass ends with it)
+  std::vector<char> flush_at;     // per operator: its layer closes a side-stream group
   // Weight gradients run on a second stream of the library's own (default
-  // priority), forked per layer once its output gradient is final and
-  // joined before the step ends, so they overlap the data-gradient chain.
+  // priority), forked in groups of layers whose output gradients are
+  // final and joined before the step ends, so they overlap the
+  // data-gradient chain.
   hipStream_t side = nullptr;
   std::vector<hipEvent_t> fork_ev;  // per operator (conv layers only)
   hipEvent_t join_ev = nullptr;
@@ -751,11 +760,8 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
     return CB_OK;
   };
   // Layers whose dY is final wait in `pending` and go to the side stream
-  // together behind one fork event, every FORK_GROUP layers: each fork is
-  // an event record on the caller's stream and a barrier packet on the
-  // side stream (ResNet-32, k=4, b=32: one fork per layer 90.3k images/s,
-  // per two layers 93.1k, per three 93.2k, per four 92.5k).
-  constexpr int FORK_GROUP = 2;
+  // together behind one fork event, in the groups of FORK_GROUP layers
+  // that flush_at marks.
   std::vector<int> pending;
   auto flush = [&](int at) -> int {
     if (pending.empty()) return CB_OK;
@@ -828,7 +834,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
           if (int rc = wgrad(i, s)) return rc;
         } else {
           pending.push_back(i);
-          if ((int)pending.size() >= FORK_GROUP)
+          if (c->flush_at[i])
             if (int rc = flush(i)) return rc;
         }
         if (o.need_dx && !o.head) {  // a head FC's dx comes from the fused head
@@ -1016,25 +1022,59 @@ void build_split_tables(cb_ctx* c) {
   c->split_tables.clear();
   c->split_bytes.clear();
   c->split_after.clear();
+  const int nops = (int)c->p.ops.size();
   const bool per_layer =
       (int64_t)c->p.k * c->p.b * c->p.m.in_h * c->p.m.in_w >= (int64_t)128 * 32 * 32;
   c->split_per_layer = per_layer;
   c->first_conv = -1;
-  for (int i = 0; i < (int)c->p.ops.size() && c->first_conv < 0; ++i)
+  for (int i = 0; i < nops && c->first_conv < 0; ++i)
     if (c->p.ops[i].kind == OP_CONV) c->first_conv = i;
-  for (int i = 0; i < (int)c->p.ops.size(); ++i) {
-    const Op& o = c->p.ops[i];
-    if (o.kind != OP_CONV || o.splits <= 1) continue;
-    if (c->split_tables.empty() || c->split_tables.back().nseg == MAX_SPLIT_SEGS || per_layer) {
-      c->split_tables.emplace_back();
-      c->split_tables.back().pstride = c->p.Pp;
-      c->split_bytes.push_back(0.0);
-      c->split_after.push_back(i);  // the group's first layer: its last weight gradient
+  // Side-stream groups: conv layers in backward order, FORK_GROUP at a time
+  // (with per-layer reductions, the first layer runs on the caller's
+  // stream instead and belongs to none).
+  c->flush_at.assign(nops, 0);
+  int in_group = 0;
+  for (int i = nops - 1; i >= 0; --i) {
+    if (c->p.ops[i].kind != OP_CONV || (per_layer && i == c->first_conv)) continue;
+    if (++in_group == FORK_GROUP) {
+      c->flush_at[i] = 1;
+      in_group = 0;
     }
+  }
+  auto add = [&](int i) {
+    const Op& o = c->p.ops[i];
     const int64_t wn = (int64_t)o.Co * o.Ci * o.R * o.R;
     split_table_add(c->split_tables.back(), c->at<float>(o.part_off), c->G() + o.w_off, wn,
                     o.splits);
     c->split_bytes.back() += 4.0 * c->p.k * wn * (o.splits + 1.0);
+  };
+  auto open = [&]() {
+    c->split_tables.emplace_back();
+    c->split_tables.back().pstride = c->p.Pp;
+    c->split_bytes.push_back(0.0);
+    c->split_after.push_back(-1);
+  };
+  if (per_layer) {
+    // one table per layer, reduced right after its weight gradient (one
+    // table per side-stream group instead, reduced after the group's last
+    // weight gradient, measured 3.7% slower at ResNet-32 k=4 b=32)
+    for (int i = 0; i < nops; ++i) {
+      if (c->p.ops[i].kind != OP_CONV || c->p.ops[i].splits <= 1) continue;
+      open();
+      add(i);
+      c->split_after.back() = i;
+    }
+    return;
+  }
+  // all layers in as few tables as fit, reduced after the backward pass
+  for (int i = 0; i < nops; ++i) {
+    const Op& o = c->p.ops[i];
+    if (o.kind != OP_CONV || o.splits <= 1) continue;
+    if (c->split_tables.empty() || c->split_tables.back().nseg == MAX_SPLIT_SEGS) {
+      open();
+      c->split_after.back() = i;  // the table's first layer: its last weight gradient
+    }
+    add(i);
   }
 }
 

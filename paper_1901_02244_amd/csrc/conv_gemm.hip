@@ -657,7 +657,8 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
 // for every segment of the table.  A block covers 64 elements of one
 // segment and one replica; its 4 waves take the splits in 4 contiguous
 // runs (loads U at a time, adds in order), combined in run order.
-__global__ __launch_bounds__(256) void reduce_splits_k(SplitTable t) {
+template <int S>
+__global__ __launch_bounds__(256) void reduce_splits_k(SplitTableT<S> t) {
   __shared__ float red[4][64];
   const int bx = blockIdx.x, j = blockIdx.y, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int lo = 0, hi = t.nseg - 1;  // the last segment whose first block is <= bx
@@ -987,7 +988,16 @@ hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char
 
 hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s) {
   if (t.nseg < 1 || t.nseg > MAX_SPLIT_SEGS) return hipErrorInvalidValue;
-  klaunch(reduce_splits_k, dim3(t.blocks, k), dim3(256), 0, s, t);
+  if (t.nseg <= SMALL_SPLIT_SEGS) {
+    SplitTableT<SMALL_SPLIT_SEGS> u;
+    u.nseg = t.nseg;
+    u.blocks = t.blocks;
+    u.pstride = t.pstride;
+    for (int i = 0; i < t.nseg; ++i) u.seg[i] = t.seg[i];
+    klaunch(reduce_splits_k<SMALL_SPLIT_SEGS>, dim3(u.blocks, k), dim3(256), 0, s, u);
+  } else {
+    klaunch(reduce_splits_k<MAX_SPLIT_SEGS>, dim3(t.blocks, k), dim3(256), 0, s, t);
+  }
   return hipGetLastError();
 }
 

@@ -159,11 +159,16 @@ struct SplitSeg {
   int splits;
   int block0;            // first 64-element block of this segment
 };
-struct SplitTable {
+template <int S>
+struct SplitTableT {
   int nseg = 0, blocks = 0;
   int64_t pstride = 0;
-  SplitSeg seg[MAX_SPLIT_SEGS];
+  SplitSeg seg[S];
 };
+using SplitTable = SplitTableT<MAX_SPLIT_SEGS>;
+// Tables of at most this many layers launch with a short kernel argument
+// (the full table is 2.6 KB, which the host copies on every launch).
+constexpr int SMALL_SPLIT_SEGS = 4;
 void split_table_add(SplitTable& t, const float* partial, float* dw, int64_t n, int splits);
 hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s);
 // db[j][c] = sum over replica j's images and pixels of dy[n][c][p].
