@@ -756,7 +756,7 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
     for (size_t t = 0; t < c->split_tables.size(); ++t)
       if (c->split_after[t] == idx)
         CB_LAUNCH(c, "reduce_splits_k", 0.0, c->split_bytes[t],
-                  reduce_splits(c->split_tables[t], k, ss));
+                  reduce_splits(c->split_tables[t], k, ss, &nm_));
     return CB_OK;
   };
   // Layers whose dY is final wait in `pending` and go to the side stream

@@ -986,7 +986,8 @@ hipError_t conv_bwd_weight(const ConvBwdWeightArgs& a, hipStream_t s, const char
   }
 }
 
-hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s) {
+static_assert(SMALL_SPLIT_SEGS == 4 && MAX_SPLIT_SEGS == 80, "the kernel names below");
+hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s, const char** name) {
   if (t.nseg < 1 || t.nseg > MAX_SPLIT_SEGS) return hipErrorInvalidValue;
   if (t.nseg <= SMALL_SPLIT_SEGS) {
     SplitTableT<SMALL_SPLIT_SEGS> u;
@@ -995,8 +996,10 @@ hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s) {
     u.pstride = t.pstride;
     for (int i = 0; i < t.nseg; ++i) u.seg[i] = t.seg[i];
     klaunch(reduce_splits_k<SMALL_SPLIT_SEGS>, dim3(u.blocks, k), dim3(256), 0, s, u);
+    if (name) *name = "reduce_splits_k<4>";
   } else {
     klaunch(reduce_splits_k<MAX_SPLIT_SEGS>, dim3(t.blocks, k), dim3(256), 0, s, t);
+    if (name) *name = "reduce_splits_k<80>";
   }
   return hipGetLastError();
 }

@@ -170,7 +170,7 @@ using SplitTable = SplitTableT<MAX_SPLIT_SEGS>;
 // (the full table is 2.6 KB, which the host copies on every launch).
 constexpr int SMALL_SPLIT_SEGS = 4;
 void split_table_add(SplitTable& t, const float* partial, float* dw, int64_t n, int splits);
-hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s);
+hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s, const char** name = nullptr);
 // db[j][c] = sum over replica j's images and pixels of dy[n][c][p].
 hipError_t channel_sum(const float* dy, int k, int b, int C, int HW, float* db,
                        int64_t pstride, hipStream_t s);
