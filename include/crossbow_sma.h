@@ -259,10 +259,14 @@ int cb_test_maxpool(int N, int C, int H, int W, int K, int stride, int pad, cons
  * xh = (bn_x - mean) * istd, per replica and channel the partial sums of d
  * and d*xh are written to bn_part [k][Ci][parts][2] (fp64), parts =
  * cb_test_conv_dgrad_parts(); their sum over parts is the total.  bn_gamma
- * (optional, with bn_y; gamma and beta at bn_gamma + j*pstride + [0, Ci) and
- * [Ci, 2Ci)) lets the implicit-GEMM epilogue take bn_y > 0 as
- * fmaf(gamma, xh, beta) > 0 instead of reading bn_y: bn_y must agree.  Same
- * kernels and tile choices as cb_step; device pointers 16-byte aligned. */
+ * (optional; gamma and beta at bn_gamma + j*pstride + [0, Ci) and [Ci, 2Ci))
+ * lets a kernel take a ReLU decision as fmaf(gamma, xh, beta) > 0 instead of
+ * reading it: with bn_y, the implicit-GEMM epilogue and the direct stride-1
+ * kernels do so for bn_y > 0; without bn_y, mask is taken to be the norm's
+ * own ReLU output and the direct stride-1 kernels do so for mask > 0 (the
+ * tensor given must agree; bn_gamma with neither bn_y nor mask is
+ * CB_EINVAL).  Same kernels and tile choices as cb_step; device pointers
+ * 16-byte aligned. */
 int cb_test_conv_dgrad_parts(int k, int b, int Ci, int H, int W, int Co, int R, int stride,
                              int pad);
 int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int stride, int pad,

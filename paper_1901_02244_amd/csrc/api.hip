@@ -865,19 +865,29 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
             // When that ReLU output is this layer's input, the ReLU mask has
             // already zeroed dX wherever it is not positive: the batch norm's
             // own ReLU test would repeat it on the same tensor.
-            if (d.bn_y == d.mask) d.bn_y = nullptr;
+            if (d.bn_y == d.mask) {
+              d.bn_y = nullptr;
+              d.mask_from_bn = d.bn_gamma != nullptr;
+            }
           }
           ProfScope ps(c);
           const char* nm = "conv_bwd_data_k";
           CB_HIP(c, conv_bwd_data(d, s, &nm));
           // every tensor the kernel and its fused epilogue must move once: dY,
-          // the filters, dX (read too when accumulating), the ReLU mask, the
-          // residual gradient and the next batch norm's x (and y for its ReLU)
-          double moved = yout + k * wn + xin * (1.0 + o.dx_accumulate + o.dx_mask);
+          // the filters, dX (read too when accumulating), the ReLU mask
+          // (unless the direct kernel recomputes it), the residual gradient
+          // and the next batch norm's x (and y for its ReLU)
+          const bool mask_read =
+              o.dx_mask && !(d.mask_from_bn && conv_direct_bwd_data_ok(g));
+          double moved = yout + k * wn + xin * (1.0 + o.dx_accumulate + mask_read);
           if (o.add_mode == ADD_SAME) moved += xin;
           if (o.add_mode == ADD_SUBSAMPLE)
             moved += (double)N * o.add_C * (o.H / o.add_st) * (o.W / o.add_st);
-          if (d.bn_part) moved += xin * (d.bn_y ? 2.0 : 1.0);
+          // (y is not read where the ReLU decision is recomputed from x:
+          // the direct stride-1 and implicit-GEMM kernels, given gamma)
+          const bool y_read = d.bn_y && !(d.bn_gamma && (conv_direct_bwd_data_ok(g) ||
+                                                          !conv_s2_dgrad_ok(g)));
+          if (d.bn_part) moved += xin * (y_read ? 2.0 : 1.0);
           ps.done(nm, flops, 4.0 * moved);
         }
         break;

@@ -83,10 +83,18 @@ struct DirectArgs {
   const float* bn_y;
   const float* bn_mean;
   const float* bn_istd;
+  const float* bn_gamma;  // RC: replica 0 gamma [Cout], beta at + Cout
+  int rc_mask;            // RC: the decision also zeroes dX (the mask's role)
 };
 
-template <int WW, int TH, int BN, int CC, bool FLIP>
+// RC (data gradient only): the batch norm has a ReLU and no residual input,
+// so the epilogue takes that ReLU's decision as bn_affine of bn_x, which it
+// reads anyway, instead of reading the norm's output (bn_y's role, for the
+// partial sums) or, when that output is this layer's input, the mask
+// (rc_mask: the decision also zeroes dX).
+template <int WW, int TH, int BN, int CC, bool FLIP, bool RC>
 __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
+  static_assert(FLIP || !RC, "the mask recompute belongs to the data gradient");
   constexpr int WP = WW + 2, HR = TH + 2;
   constexpr int NPIX = HR * WP;           // pixels of the input tile (with border)
   constexpr int M = TH * WW;              // output pixels per tile
@@ -252,7 +260,7 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
         if (a.mask) m[t][u] = *reinterpret_cast<const v4f*>(a.mask + g);
         if (a.bn_part) {
           x[t][u] = *reinterpret_cast<const v4f*>(a.bn_x + g);
-          if (a.bn_y) y[t][u] = *reinterpret_cast<const v4f*>(a.bn_y + g);
+          if (!RC && a.bn_y) y[t][u] = *reinterpret_cast<const v4f*>(a.bn_y + g);
         }
       }
   };
@@ -272,6 +280,11 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       if (FLIP && a.bn_part) {
         bm = a.bn_mean[d.j * a.Cout + co];
         bi = a.bn_istd[d.j * a.Cout + co];
+      }
+      float ga = 0.f, be = 0.f;
+      if (RC) {
+        ga = a.bn_gamma[(int64_t)d.j * a.pstride + co];
+        be = a.bn_gamma[(int64_t)d.j * a.pstride + a.Cout + co];
       }
 #pragma unroll
       for (int t = 0; t < TM; ++t) {
@@ -302,15 +315,25 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
                                ih / st) * ((WW + st - 1) / st) + iw / st];
             }
           }
-          if (a.mask)
+          bool r[4];
+          if (RC)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) r[i] = bn_affine(e_x[t][u][i], bm, bi, ga, be) > 0.f;
+          if (RC && a.rc_mask) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (!r[i]) v[i] = 0.f;
+          } else if (a.mask) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
               if (!(e_mask[t][u][i] > 0.f)) v[i] = 0.f;
+          }
           *reinterpret_cast<v4f*>(a.out + g) = v;
           if (a.bn_part) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const float dd = (!a.bn_y || e_y[t][u][i] > 0.f) ? v[i] : 0.f;
+              const bool keep = RC ? r[i] : (!a.bn_y || e_y[t][u][i] > 0.f);
+              const float dd = keep ? v[i] : 0.f;
               const float xh = (e_x[t][u][i] - bm) * bi;
               s1[u] += (double)dd;
               s2[u] += (double)dd * xh;
@@ -849,15 +872,16 @@ hipError_t launch_s2(const DirectArgs& a, hipStream_t s, const char** name) {
   return hipGetLastError();
 }
 
-template <int WW, int TH, int BN, int CC, bool FLIP>
+template <int WW, int TH, int BN, int CC, bool FLIP, bool RC>
 const char* direct_name() {
   static const std::string n = std::string("conv3x3_k<") + std::to_string(WW) + ", " +
                                std::to_string(TH) + ", " + std::to_string(BN) + ", " +
-                               std::to_string(CC) + ", " + (FLIP ? "true" : "false") + ">";
+                               std::to_string(CC) + ", " + (FLIP ? "true" : "false") + ", " +
+                               (RC ? "true" : "false") + ">";
   return n.c_str();
 }
 
-template <int WW, int TH, int BN, int CC, bool FLIP>
+template <int WW, int TH, int BN, int CC, bool FLIP, bool RC>
 hipError_t launch(const DirectArgs& a, hipStream_t s, const char** name) {
   // as many workgroups as are resident at once, each taking an equal share
   // of the tiles (the last share may be one short)
@@ -866,16 +890,16 @@ hipError_t launch(const DirectArgs& a, hipStream_t s, const char** name) {
     int per_cu = 0, cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv3x3_k<WW, TH, BN, CC, FLIP>, 256,
-                                                     0) != hipSuccess)
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv3x3_k<WW, TH, BN, CC, FLIP, RC>,
+                                                     256, 0) != hipSuccess)
       return hipErrorInvalidValue;
     resident = std::max(1, per_cu) * std::max(1, cus);
   }
   const int64_t T = (int64_t)a.k * a.b * (a.H / TH) * (a.Cout / BN);
   const int64_t per = (T + resident - 1) / resident;
   const int64_t G = (T + per - 1) / per;
-  klaunch(conv3x3_k<WW, TH, BN, CC, FLIP>, dim3((unsigned)G), dim3(256), 0, s, a);
-  if (name) *name = direct_name<WW, TH, BN, CC, FLIP>();
+  klaunch(conv3x3_k<WW, TH, BN, CC, FLIP, RC>, dim3((unsigned)G), dim3(256), 0, s, a);
+  if (name) *name = direct_name<WW, TH, BN, CC, FLIP, RC>();
   return hipGetLastError();
 }
 
@@ -904,23 +928,23 @@ DirectTile direct_pick(int k, int b, int W, int Cout) {
   return {th_min, 16};
 }
 
-template <bool FLIP, int WW>
+template <bool FLIP, bool RC, int WW>
 hipError_t dispatch_w(const DirectArgs& a, DirectTile t, hipStream_t s, const char** name) {
   constexpr int TH1 = WW == 32 ? 4 : 8, TH2 = WW == 32 ? 2 : (WW == 16 ? 4 : 8);
   if (t.th == TH1) {
-    if (t.bn == 32) return launch<WW, TH1, 32, 16, FLIP>(a, s, name);
-    return launch<WW, TH1, 16, 16, FLIP>(a, s, name);
+    if (t.bn == 32) return launch<WW, TH1, 32, 16, FLIP, RC>(a, s, name);
+    return launch<WW, TH1, 16, 16, FLIP, RC>(a, s, name);
   }
-  if (t.bn == 32) return launch<WW, TH2, 32, 16, FLIP>(a, s, name);
-  return launch<WW, TH2, 16, 16, FLIP>(a, s, name);
+  if (t.bn == 32) return launch<WW, TH2, 32, 16, FLIP, RC>(a, s, name);
+  return launch<WW, TH2, 16, 16, FLIP, RC>(a, s, name);
 }
 
-template <bool FLIP>
+template <bool FLIP, bool RC>
 hipError_t dispatch(const DirectArgs& a, int W, hipStream_t s, const char** name) {
   const DirectTile t = direct_pick(a.k, a.b, W, a.Cout);
-  if (W == 32) return dispatch_w<FLIP, 32>(a, t, s, name);
-  if (W == 16) return dispatch_w<FLIP, 16>(a, t, s, name);
-  return dispatch_w<FLIP, 8>(a, t, s, name);
+  if (W == 32) return dispatch_w<FLIP, RC, 32>(a, t, s, name);
+  if (W == 16) return dispatch_w<FLIP, RC, 16>(a, t, s, name);
+  return dispatch_w<FLIP, RC, 8>(a, t, s, name);
 }
 
 // Weight gradient: units of 4 rows (8 at width 8), so that a workgroup
@@ -1010,7 +1034,7 @@ hipError_t conv_direct_fwd(const ConvFwdArgs& f, hipStream_t s, const char** nam
   a.in = f.x; a.w = f.w; a.pstride = f.pstride; a.out = f.y;
   a.bias = f.bias; a.relu = f.relu; a.stats = f.stats;
   a.add_mode = ADD_NONE;
-  return dispatch<false>(a, f.g.W, s, name);
+  return dispatch<false, false>(a, f.g.W, s, name);
 }
 
 hipError_t conv_direct_bwd_data(const ConvBwdDataArgs& d, hipStream_t s, const char** name) {
@@ -1022,7 +1046,14 @@ hipError_t conv_direct_bwd_data(const ConvBwdDataArgs& d, hipStream_t s, const c
   a.add = d.add; a.add_mode = d.add_mode; a.add_C = d.add_C; a.add_st = d.add_st;
   a.bn_part = d.bn_part; a.bn_x = d.bn_x; a.bn_y = d.bn_y;
   a.bn_mean = d.bn_mean; a.bn_istd = d.bn_istd;
-  return dispatch<true>(a, d.g.W, s, name);
+  if (d.bn_gamma && d.bn_part && d.bn_x && (d.bn_y || (d.mask_from_bn && d.mask))) {
+    a.bn_gamma = d.bn_gamma;
+    a.rc_mask = !d.bn_y;
+    if (a.rc_mask) a.mask = nullptr;
+    a.bn_y = nullptr;
+    return dispatch<true, true>(a, d.g.W, s, name);
+  }
+  return dispatch<true, false>(a, d.g.W, s, name);
 }
 
 }  // namespace cbk

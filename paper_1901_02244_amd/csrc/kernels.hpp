@@ -87,15 +87,19 @@ struct ConvBwdDataArgs {
   // with d = dx masked where the norm's ReLU output bn_y is not positive
   // (bn_y null: no mask) and xh = (bn_x - mean) * istd: sum d and sum
   // d*xh, [k][Ci][tiles_m][2].  For a norm with no residual input the
-  // caller may also give bn_gamma: the implicit-GEMM epilogue then
-  // recomputes the ReLU output as bn_affine of bn_x instead of reading
-  // bn_y (the direct kernels read bn_y).
+  // caller may also give bn_gamma: the implicit-GEMM epilogue and the
+  // direct stride-1 kernels then recompute the ReLU output's sign as
+  // bn_affine of bn_x instead of reading bn_y.
   double* bn_part;
   const float* bn_x;
   const float* bn_y;
   const float* bn_mean;
   const float* bn_istd;
   const float* bn_gamma = nullptr;  // replica 0 gamma [Ci], beta at + Ci; pstride apart
+  // The mask is that norm's own ReLU output (bn_y null, bn_gamma given):
+  // the direct kernels then take the mask's decision as bn_affine of bn_x
+  // instead of reading the mask.
+  bool mask_from_bn = false;
 };
 
 struct ConvBwdWeightArgs {

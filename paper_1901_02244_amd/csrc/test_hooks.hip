@@ -123,7 +123,7 @@ int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int st
   if (!geom_ok(k, b, Ci, H, W, Co, R, stride, pad) || !conv_supported(R, R, stride, true) ||
       !dy || !params || !dx || add_mode < ADD_NONE || add_mode > ADD_SUBSAMPLE ||
       (add_mode != ADD_NONE && !add) || (bn_part && (!bn_x || !bn_mean || !bn_istd)) ||
-      (bn_gamma && !bn_y))
+      (bn_gamma && !bn_y && !mask))
     return CB_EINVAL;
   ConvBwdDataArgs d;
   d.g = make_geom(k, b, Ci, H, W, Co, R, stride, pad);
@@ -143,6 +143,7 @@ int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int st
   d.bn_mean = bn_mean;
   d.bn_istd = bn_istd;
   d.bn_gamma = bn_gamma;
+  d.mask_from_bn = bn_gamma && !bn_y;
   return rc_of(conv_bwd_data(d, static_cast<hipStream_t>(stream)));
 }
 

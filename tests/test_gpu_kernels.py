@@ -343,7 +343,9 @@ def test_softmax_xent_kernel(case):
 
 
 # (name, k, b, Ci, H, Co, R, stride, pad, accumulate, mask, add_mode, add_C, bn, bn_y:
-#  0 none, 1 a y tensor, 2 a y tensor that gamma and beta recompute from bn_x)
+#  0 none, 1 a y tensor, 2 a y tensor that gamma and beta recompute from bn_x,
+#  3 no y: the mask is the norm's own ReLU output, recomputed from bn_x by the
+#  direct stride-1 kernels and read by the others)
 DGRAD_EPILOGUE = [
     ("direct.w32.same.bn", 2, 4, 16, 32, 16, 3, 1, 1, 1, 1, 1, 16, 1, 1),
     ("direct.w16.bn", 2, 3, 32, 16, 32, 3, 1, 1, 0, 0, 0, 0, 1, 1),
@@ -363,6 +365,11 @@ DGRAD_EPILOGUE = [
     ("gemm.3x3s2.ragged.bn.relux", 2, 3, 7, 13, 19, 3, 2, 1, 0, 0, 0, 0, 1, 2),
     ("gemm.5x5.bn.relux", 2, 4, 6, 14, 16, 5, 1, 0, 0, 0, 0, 0, 1, 2),
     ("gemm.1x1s2.grid.acc.same.bn.relux", 2, 3, 24, 14, 40, 1, 2, 0, 1, 0, 1, 24, 1, 2),
+    ("direct.w32.mask.bn.rc", 2, 4, 16, 32, 16, 3, 1, 1, 0, 1, 0, 0, 1, 3),
+    ("direct.w16.acc.mask.same.bn.rc", 2, 3, 32, 16, 32, 3, 1, 1, 1, 1, 1, 32, 1, 3),
+    ("direct.w8.mask.bn.rc", 2, 3, 64, 8, 64, 3, 1, 1, 0, 1, 0, 0, 1, 3),
+    ("s2.w16.mask.bn.rc", 2, 4, 32, 16, 64, 3, 2, 1, 0, 1, 0, 0, 1, 3),
+    ("gemm.5x5.mask.bn.rc", 2, 4, 6, 14, 16, 5, 1, 0, 0, 1, 0, 0, 1, 3),
 ]
 
 
@@ -400,18 +407,22 @@ def test_conv_data_gradient_epilogue(case):
     for j in range(k):
         gb[j * pstride:j * pstride + Ci] = 1 + 0.3 * rng.standard_normal(Ci)
         gb[j * pstride + Ci:j * pstride + 2 * Ci] = 0.5 * rng.standard_normal(Ci)
-    if bn and use_y == 2:
-        bn_y = np.concatenate([np.where(
+    if bn and use_y in (2, 3):
+        sign = np.concatenate([np.where(
             _bn_relu_from_x(bn_x[j * b:(j + 1) * b], mean[j], istd[j],
                             gb[j * pstride:j * pstride + Ci],
                             gb[j * pstride + Ci:j * pstride + 2 * Ci]), 1.0, -1.0)
             for j in range(k)]).astype(np.float32)
+        if use_y == 2:
+            bn_y = sign
+        else:
+            mask = sign
     L = cb.lib()
     parts = L.cb_test_conv_dgrad_parts(k, b, Ci, H, H, Co, R, st, pad)
     assert parts > 0
     d = {n_: (_dev(v) if v is not None else None) for n_, v in
          dict(dy=dy, p=params, dx=dx0, mask=mask, add=add, x=bn_x, y=bn_y, mean=mean,
-              istd=istd, g=gb if (bn and use_y == 2) else None).items()}
+              istd=istd, g=gb if (bn and use_y in (2, 3)) else None).items()}
     part = torch.zeros(k * Ci * parts * 2, dtype=torch.float64, device="cuda") if bn else None
     ptr = lambda t: t.data_ptr() if t is not None else None
     rc = L.cb_test_conv_dgrad(k, b, Ci, H, H, Co, R, st, pad, ptr(d["dy"]), ptr(d["p"]), pstride,
