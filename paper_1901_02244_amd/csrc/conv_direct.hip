@@ -949,14 +949,19 @@ hipError_t dispatch(const DirectArgs& a, int W, hipStream_t s, const char** name
 
 // Weight gradient: units of 4 rows (8 at width 8), so that a workgroup
 // has several units to pipeline; the split gives every CU two workgroups
-// over all replicas and channel blocks where the units allow.
+// over all replicas and channel blocks where the units allow.  With at
+// most 128 images per step it gives one per CU: the weight gradients run
+// beside the data-gradient chain, whose kernels are then small, and leave
+// it the other slots (ResNet-32 k=4 b=32 +0.5%, k=2..8 at b=16 +0.5-3%,
+// one replica of 128 +3.4%; at k=16 and 32, b=16, one per CU lost 1-2%).
 constexpr int WG_TH32 = 4, WG_TH16 = 4, WG_TH8 = 8;
 int wgrad_th(int W) { return W == 32 ? WG_TH32 : W == 16 ? WG_TH16 : WG_TH8; }
 
 void wgrad_split(const ConvGeom& g, int* splits, int* per) {
   const int units = g.b * (g.H / wgrad_th(g.W));
   const int64_t blocks = (int64_t)g.k * (g.Co / 16) * (g.Ci / 16);
-  int sp = (int)std::max<int64_t>(1, std::min<int64_t>(units, (DIRECT_MIN_WGS + blocks - 1) / blocks));
+  const int64_t wgs = (int64_t)g.k * g.b <= 128 ? DIRECT_MIN_WGS / 2 : DIRECT_MIN_WGS;
+  int sp = (int)std::max<int64_t>(1, std::min<int64_t>(units, (wgs + blocks - 1) / blocks));
   const int pr = (units + sp - 1) / sp;
   *per = pr;
   *splits = (units + pr - 1) / pr;
