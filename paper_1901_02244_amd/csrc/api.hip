@@ -461,8 +461,9 @@ struct ProfAgg {
 // one fork event: each fork is an event record on the caller's stream and a
 // barrier packet on the side stream (ResNet-32, k=4, b=32: one fork per
 // layer 90.3k images/s, per two layers 93.1k, per three 93.2k, per four
-// 92.5k).
-constexpr int FORK_GROUP = 2;
+// 92.5k; with the lighter weight-gradient grids, three layers per fork
+// matched two at k=4 b=32 and were 2% faster at k=1..4, b=16).
+constexpr int FORK_GROUP = 3;
 
 struct cb_ctx {
   Plan p;
