@@ -92,10 +92,15 @@ struct DirectArgs {
 // reads anyway, instead of reading the norm's output (bn_y's role, for the
 // partial sums) or, when that output is this layer's input, the mask
 // (rc_mask: the decision also zeroes dX).
-template <int WW, int TH, int BN, int CC, bool FLIP, bool RC>
+// ST (forward only): the convolution's stride.  WW and a.H are the output's
+// width and height; the input is ST times as wide and high, and its tile
+// spans (TH - 1) ST + 3 rows of (WW - 1) ST + 3 pixels.
+template <int WW, int TH, int BN, int CC, bool FLIP, bool RC, int ST>
 __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   static_assert(FLIP || !RC, "the mask recompute belongs to the data gradient");
-  constexpr int WP = WW + 2, HR = TH + 2;
+  static_assert(ST == 1 || (ST == 2 && !FLIP), "stride 2 is a forward tile");
+  constexpr int WI = WW * ST;             // input width
+  constexpr int WP = (WW - 1) * ST + 3, HR = (TH - 1) * ST + 3;
   constexpr int NPIX = HR * WP;           // pixels of the input tile (with border)
   constexpr int M = TH * WW;              // output pixels per tile
   constexpr int TM = M / 64;              // 16-pixel blocks per wave (waves split M)
@@ -127,7 +132,8 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   __shared__ double red[4][BN][2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4;
-  const int H = a.H, HW = H * WW;
+  const int H = a.H, HW = H * WW;         // output plane
+  const int HI = H * ST, HWI = HI * WI;   // input plane
   const int tiles_img = H / TH;
   const int rows_rep = a.b * tiles_img;            // row tiles of one replica
   const int per_rep = rows_rep * (a.Cout / BN);    // tiles of one replica
@@ -153,8 +159,8 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
 
   v4f rx[NXT], rw[NWT];
   auto load = [&](const Tile& d, int c0) {
-    const auto src = buf_rsrc(a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HW,
-                              (uint32_t)(a.Cin * HW * 4));
+    const auto src = buf_rsrc(a.in + ((int64_t)(d.j * a.b + d.img) * a.Cin) * HWI,
+                              (uint32_t)(a.Cin * HWI * 4));
     const auto wsrc = buf_rsrc(a.w + (int64_t)d.j * a.pstride, (uint32_t)(a.Cin * a.Cout * 36));
 #pragma unroll
     for (int u = 0; u < NXT; ++u) {
@@ -163,12 +169,12 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
       // coalesced along the image row
       const int e = tid + u * 256;
       const int c4 = e / NPIX, pix = e - c4 * NPIX, hr = pix / WP, wc = pix - hr * WP;
-      const int ih = d.oh0 - 1 + hr, iw = wc - 1;
-      const bool ok = (NX % 256 == 0 || e < NX) && (unsigned)ih < (unsigned)H &&
-                      (unsigned)iw < (unsigned)WW;
-      const uint32_t o = (uint32_t)(((c0 + 4 * c4) * HW + ih * WW + iw) * 4);
+      const int ih = d.oh0 * ST - 1 + hr, iw = wc - 1;
+      const bool ok = (NX % 256 == 0 || e < NX) && (unsigned)ih < (unsigned)HI &&
+                      (unsigned)iw < (unsigned)WI;
+      const uint32_t o = (uint32_t)(((c0 + 4 * c4) * HWI + ih * WI + iw) * 4);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) rx[u][q] = buf_ld(src, ok ? o + (uint32_t)(q * HW * 4) : OUTSIDE);
+      for (int q = 0; q < 4; ++q) rx[u][q] = buf_ld(src, ok ? o + (uint32_t)(q * HWI * 4) : OUTSIDE);
     }
 #pragma unroll
     for (int u = 0; u < NWT; ++u) {
@@ -235,7 +241,7 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   for (int t = 0; t < TM; ++t) {
     const int m = (wave * TM + t) * 16 + (lane & 15);
     const int ohl = m / WW, ow = m - ohl * WW;
-    xbase[t] = (ohl * WP + ow) * PS + 4 * kq;
+    xbase[t] = (ohl * ST * WP + ow * ST) * PS + 4 * kq;
   }
   const int wbase = (lane & 15) * WS + 4 * kq;
 
@@ -872,16 +878,16 @@ hipError_t launch_s2(const DirectArgs& a, hipStream_t s, const char** name) {
   return hipGetLastError();
 }
 
-template <int WW, int TH, int BN, int CC, bool FLIP, bool RC>
+template <int WW, int TH, int BN, int CC, bool FLIP, bool RC, int ST>
 const char* direct_name() {
   static const std::string n = std::string("conv3x3_k<") + std::to_string(WW) + ", " +
                                std::to_string(TH) + ", " + std::to_string(BN) + ", " +
                                std::to_string(CC) + ", " + (FLIP ? "true" : "false") + ", " +
-                               (RC ? "true" : "false") + ">";
+                               (RC ? "true" : "false") + ", " + std::to_string(ST) + ">";
   return n.c_str();
 }
 
-template <int WW, int TH, int BN, int CC, bool FLIP, bool RC>
+template <int WW, int TH, int BN, int CC, bool FLIP, bool RC, int ST>
 hipError_t launch(const DirectArgs& a, hipStream_t s, const char** name) {
   // as many workgroups as are resident at once, each taking an equal share
   // of the tiles (the last share may be one short)
@@ -890,16 +896,16 @@ hipError_t launch(const DirectArgs& a, hipStream_t s, const char** name) {
     int per_cu = 0, cus = 0, dev = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, conv3x3_k<WW, TH, BN, CC, FLIP, RC>,
-                                                     256, 0) != hipSuccess)
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu, conv3x3_k<WW, TH, BN, CC, FLIP, RC, ST>, 256, 0) != hipSuccess)
       return hipErrorInvalidValue;
     resident = std::max(1, per_cu) * std::max(1, cus);
   }
   const int64_t T = (int64_t)a.k * a.b * (a.H / TH) * (a.Cout / BN);
   const int64_t per = (T + resident - 1) / resident;
   const int64_t G = (T + per - 1) / per;
-  klaunch(conv3x3_k<WW, TH, BN, CC, FLIP, RC>, dim3((unsigned)G), dim3(256), 0, s, a);
-  if (name) *name = direct_name<WW, TH, BN, CC, FLIP, RC>();
+  klaunch(conv3x3_k<WW, TH, BN, CC, FLIP, RC, ST>, dim3((unsigned)G), dim3(256), 0, s, a);
+  if (name) *name = direct_name<WW, TH, BN, CC, FLIP, RC, ST>();
   return hipGetLastError();
 }
 
@@ -928,23 +934,25 @@ DirectTile direct_pick(int k, int b, int W, int Cout) {
   return {th_min, 16};
 }
 
-template <bool FLIP, bool RC, int WW>
+template <bool FLIP, bool RC, int ST, int WW>
 hipError_t dispatch_w(const DirectArgs& a, DirectTile t, hipStream_t s, const char** name) {
   constexpr int TH1 = WW == 32 ? 4 : 8, TH2 = WW == 32 ? 2 : (WW == 16 ? 4 : 8);
   if (t.th == TH1) {
-    if (t.bn == 32) return launch<WW, TH1, 32, 16, FLIP, RC>(a, s, name);
-    return launch<WW, TH1, 16, 16, FLIP, RC>(a, s, name);
+    if (t.bn == 32) return launch<WW, TH1, 32, 16, FLIP, RC, ST>(a, s, name);
+    return launch<WW, TH1, 16, 16, FLIP, RC, ST>(a, s, name);
   }
-  if (t.bn == 32) return launch<WW, TH2, 32, 16, FLIP, RC>(a, s, name);
-  return launch<WW, TH2, 16, 16, FLIP, RC>(a, s, name);
+  if (t.bn == 32) return launch<WW, TH2, 32, 16, FLIP, RC, ST>(a, s, name);
+  return launch<WW, TH2, 16, 16, FLIP, RC, ST>(a, s, name);
 }
 
-template <bool FLIP, bool RC>
+// W: the output width
+template <bool FLIP, bool RC, int ST = 1>
 hipError_t dispatch(const DirectArgs& a, int W, hipStream_t s, const char** name) {
   const DirectTile t = direct_pick(a.k, a.b, W, a.Cout);
-  if (W == 32) return dispatch_w<FLIP, RC, 32>(a, t, s, name);
-  if (W == 16) return dispatch_w<FLIP, RC, 16>(a, t, s, name);
-  return dispatch_w<FLIP, RC, 8>(a, t, s, name);
+  if constexpr (ST == 1)
+    if (W == 32) return dispatch_w<FLIP, RC, ST, 32>(a, t, s, name);
+  if (W == 16) return dispatch_w<FLIP, RC, ST, 16>(a, t, s, name);
+  return dispatch_w<FLIP, RC, ST, 8>(a, t, s, name);
 }
 
 // Weight gradient: units of 4 rows (8 at width 8), so that a workgroup
@@ -1016,8 +1024,15 @@ hipError_t conv_direct_wgrad(const ConvBwdWeightArgs& w, hipStream_t s, const ch
   return launch_wgrad<8, WG_TH8>(a, s, name);
 }
 
+// Stride 2 (forward only): square inputs of width 16 or 32 (outputs 8 or 16).
+bool direct_s2_fwd_ok(const ConvGeom& g) {
+  return g.R == 3 && g.S == 3 && g.st == 2 && g.pad == 1 && g.H == g.W && g.H % 2 == 0 &&
+         (g.W == 16 || g.W == 32) && g.Ho == g.H / 2 && g.Wo == g.W / 2 && g.Ci % 16 == 0 &&
+         g.Co % 16 == 0;
+}
+
 bool conv_direct_fwd_ok(const ConvGeom& g) {
-  return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad);
+  return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad) || direct_s2_fwd_ok(g);
 }
 
 bool conv_direct_bwd_data_ok(const ConvGeom& g) {
@@ -1025,7 +1040,7 @@ bool conv_direct_bwd_data_ok(const ConvGeom& g) {
 }
 
 int conv_direct_fwd_tiles(const ConvGeom& g) {
-  return g.b * (g.H / direct_pick(g.k, g.b, g.W, g.Co).th);
+  return g.b * (g.Ho / direct_pick(g.k, g.b, g.Wo, g.Co).th);
 }
 
 int conv_direct_bwd_data_tiles(const ConvGeom& g) {
@@ -1034,11 +1049,12 @@ int conv_direct_bwd_data_tiles(const ConvGeom& g) {
 
 hipError_t conv_direct_fwd(const ConvFwdArgs& f, hipStream_t s, const char** name) {
   DirectArgs a{};
-  a.k = f.g.k; a.b = f.g.b; a.H = f.g.H;
+  a.k = f.g.k; a.b = f.g.b; a.H = f.g.Ho;
   a.Cin = f.g.Ci; a.Cout = f.g.Co;
   a.in = f.x; a.w = f.w; a.pstride = f.pstride; a.out = f.y;
   a.bias = f.bias; a.relu = f.relu; a.stats = f.stats;
   a.add_mode = ADD_NONE;
+  if (f.g.st == 2) return dispatch<false, false, 2>(a, f.g.Wo, s, name);
   return dispatch<false, false>(a, f.g.W, s, name);
 }
 
