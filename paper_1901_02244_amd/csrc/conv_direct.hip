@@ -710,9 +710,9 @@ __global__ __launch_bounds__(256) void conv3x3s2_dgrad_k(DirectArgs a) {
 // added in wave order; the result goes to dw (one split) or to the split's
 // slot of `partial` for the fixed-order split reduction.
 struct WgradArgs {
-  int k, b, H;
+  int k, b, H;      // H: the height of dY
   int Ci, Co;
-  const float* x;   // [k*b][Ci][H][W]
+  const float* x;   // [k*b][Ci][H*ST][W*ST]
   const float* dy;  // [k*b][Co][H][W]
   float* dw;        // replica 0 gradient [Co][Ci][3][3] (splits == 1)
   int64_t pstride;
@@ -724,9 +724,12 @@ struct WgradArgs {
 // 64-lane read touches fall on (nearly) distinct banks.
 constexpr int pad34(int n) { return n + ((34 - n % 64) + 64) % 64; }
 
-template <int WW, int TH>
+// ST: the convolution's stride.  WW is dY's width; the X tile of a unit
+// spans (TH - 1) ST + 3 rows of (WW - 1) ST + 3 pixels.
+template <int WW, int TH, int ST>
 __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
-  constexpr int WP = WW + 2, HR = TH + 2;
+  constexpr int WI = WW * ST;             // X width
+  constexpr int WP = (WW - 1) * ST + 3, HR = (TH - 1) * ST + 3;
   constexpr int SA = pad34(TH * WW);      // dY tile channel stride
   constexpr int SB = pad34(HR * WP);      // X tile channel stride
   constexpr int NQ = TH * WW / 4;         // 4-pixel steps per unit
@@ -747,6 +750,7 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
   const int co0 = (blockIdx.x / nci) * 16, ci0 = (blockIdx.x % nci) * 16;
   const int split = blockIdx.y, j = blockIdx.z;
   const int H = a.H, HW = H * WW, tiles_img = H / TH;
+  const int HI = H * ST, HWI = HI * WI;
   const int units = a.b * tiles_img;
   const int u0 = split * a.per, u1 = min(units, u0 + a.per);
 
@@ -761,7 +765,7 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
     const int img = u / tiles_img, h0 = (u - img * tiles_img) * TH;
     const int n = j * a.b + img;
     const float* DY = a.dy + ((int64_t)n * a.Co + co0) * HW + h0 * WW;
-    const float* X = a.x + ((int64_t)n * a.Ci + ci0) * HW;
+    const float* X = a.x + ((int64_t)n * a.Ci + ci0) * HWI;
 #pragma unroll
     for (int i = 0; i < NA4T; ++i) {
       const int e = tid + i * 256;
@@ -770,15 +774,15 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
         ra[i] = *reinterpret_cast<const v4f*>(DY + (int64_t)c * HW + q * 4);
       }
     }
-    const auto xsrc = buf_rsrc(X, (uint32_t)(16 * HW * 4));
+    const auto xsrc = buf_rsrc(X, (uint32_t)(16 * HWI * 4));
 #pragma unroll
     for (int i = 0; i < NXT; ++i) {
       const int e = tid + i * 256;
       const int c = e / (HR * WP), rem = e - c * (HR * WP), hr = rem / WP, wc = rem - hr * WP;
-      const int ih = h0 - 1 + hr, iw = wc - 1;
-      const bool ok = (NX % 256 == 0 || e < NX) && (unsigned)ih < (unsigned)H &&
-                      (unsigned)iw < (unsigned)WW;
-      rx[i] = buf_ld(xsrc, ok ? (uint32_t)((c * HW + ih * WW + iw) * 4) : OUTSIDE);
+      const int ih = h0 * ST - 1 + hr, iw = wc - 1;
+      const bool ok = (NX % 256 == 0 || e < NX) && (unsigned)ih < (unsigned)HI &&
+                      (unsigned)iw < (unsigned)WI;
+      rx[i] = buf_ld(xsrc, ok ? (uint32_t)((c * HWI + ih * WI + iw) * 4) : OUTSIDE);
     }
   };
   auto store = [&]() {
@@ -815,7 +819,7 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
       const int q = wave + 4 * i;
       const int h = q / (WW / 4), w = (q - h * (WW / 4)) * 4;
       const float av = As[l16 * SA + h * WW + w + kq];
-      const float* xb = Bs + l16 * SB + h * WP + w + kq;
+      const float* xb = Bs + l16 * SB + (h * WP + w + kq) * ST;
       float bv[9];
 #pragma unroll
       for (int t = 0; t < 9; ++t) bv[t] = xb[(t / 3) * WP + (t % 3)];
@@ -841,13 +845,13 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
   }
 }
 
-template <int WW, int TH>
+template <int WW, int TH, int ST>
 hipError_t launch_wgrad(const WgradArgs& a, hipStream_t s, const char** name) {
   dim3 grid((unsigned)((a.Co / 16) * (a.Ci / 16)), (unsigned)a.splits, (unsigned)a.k);
-  klaunch(conv3x3_wgrad_k<WW, TH>, grid, dim3(256), 0, s, a);
+  klaunch(conv3x3_wgrad_k<WW, TH, ST>, grid, dim3(256), 0, s, a);
   if (name) {
-    static const std::string n =
-        std::string("conv3x3_wgrad_k<") + std::to_string(WW) + ", " + std::to_string(TH) + ">";
+    static const std::string n = std::string("conv3x3_wgrad_k<") + std::to_string(WW) + ", " +
+                                 std::to_string(TH) + ", " + std::to_string(ST) + ">";
     *name = n.c_str();
   }
   return hipGetLastError();
@@ -966,7 +970,7 @@ constexpr int WG_TH32 = 4, WG_TH16 = 4, WG_TH8 = 8;
 int wgrad_th(int W) { return W == 32 ? WG_TH32 : W == 16 ? WG_TH16 : WG_TH8; }
 
 void wgrad_split(const ConvGeom& g, int* splits, int* per) {
-  const int units = g.b * (g.H / wgrad_th(g.W));
+  const int units = g.b * (g.Ho / wgrad_th(g.Wo));
   const int64_t blocks = (int64_t)g.k * (g.Co / 16) * (g.Ci / 16);
   const int64_t wgs = (int64_t)g.k * g.b <= 128 ? DIRECT_MIN_WGS / 2 : DIRECT_MIN_WGS;
   int sp = (int)std::max<int64_t>(1, std::min<int64_t>(units, (wgs + blocks - 1) / blocks));
@@ -1002,8 +1006,16 @@ hipError_t conv_s2_dgrad(const ConvBwdDataArgs& d, hipStream_t s, const char** n
   return launch_s2<8, 8, 16, 16>(a, s, name);
 }
 
+// Stride 2 (forward and weight gradient): square inputs of width 16 or 32
+// (outputs 8 or 16).
+bool direct_s2_ok(const ConvGeom& g) {
+  return g.R == 3 && g.S == 3 && g.st == 2 && g.pad == 1 && g.H == g.W && g.H % 2 == 0 &&
+         (g.W == 16 || g.W == 32) && g.Ho == g.H / 2 && g.Wo == g.W / 2 && g.Ci % 16 == 0 &&
+         g.Co % 16 == 0;
+}
+
 bool conv_direct_wgrad_ok(const ConvGeom& g) {
-  return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad);
+  return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad) || direct_s2_ok(g);
 }
 
 int conv_direct_wgrad_splits(const ConvGeom& g) {
@@ -1014,25 +1026,23 @@ int conv_direct_wgrad_splits(const ConvGeom& g) {
 
 hipError_t conv_direct_wgrad(const ConvBwdWeightArgs& w, hipStream_t s, const char** name) {
   WgradArgs a{};
-  a.k = w.g.k; a.b = w.g.b; a.H = w.g.H;
+  a.k = w.g.k; a.b = w.g.b; a.H = w.g.Ho;
   a.Ci = w.g.Ci; a.Co = w.g.Co;
   a.x = w.x; a.dy = w.dy; a.dw = w.dw; a.pstride = w.pstride; a.partial = w.partial;
   wgrad_split(w.g, &a.splits, &a.per);
   if (w.splits != a.splits) return hipErrorInvalidValue;  // scratch sized for another split
-  if (w.g.W == 32) return launch_wgrad<32, WG_TH32>(a, s, name);
-  if (w.g.W == 16) return launch_wgrad<16, WG_TH16>(a, s, name);
-  return launch_wgrad<8, WG_TH8>(a, s, name);
+  if (w.g.st == 2) {
+    if (w.g.Wo == 16) return launch_wgrad<16, WG_TH16, 2>(a, s, name);
+    return launch_wgrad<8, WG_TH8, 2>(a, s, name);
+  }
+  if (w.g.W == 32) return launch_wgrad<32, WG_TH32, 1>(a, s, name);
+  if (w.g.W == 16) return launch_wgrad<16, WG_TH16, 1>(a, s, name);
+  return launch_wgrad<8, WG_TH8, 1>(a, s, name);
 }
 
-// Stride 2 (forward only): square inputs of width 16 or 32 (outputs 8 or 16).
-bool direct_s2_fwd_ok(const ConvGeom& g) {
-  return g.R == 3 && g.S == 3 && g.st == 2 && g.pad == 1 && g.H == g.W && g.H % 2 == 0 &&
-         (g.W == 16 || g.W == 32) && g.Ho == g.H / 2 && g.Wo == g.W / 2 && g.Ci % 16 == 0 &&
-         g.Co % 16 == 0;
-}
 
 bool conv_direct_fwd_ok(const ConvGeom& g) {
-  return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad) || direct_s2_fwd_ok(g);
+  return direct_ok(g.H, g.W, g.Ci, g.Co, g.R, g.st, g.pad) || direct_s2_ok(g);
 }
 
 bool conv_direct_bwd_data_ok(const ConvGeom& g) {
