@@ -914,9 +914,11 @@ hipError_t launch(const DirectArgs& a, hipStream_t s, const char** name) {
 }
 
 // Built for square images of width 8, 16 or 32 and channel counts that
-// are multiples of 16.  Tile choice: TH output rows (a multiple of 64
-// pixels) and BN output channels; the largest tile that still gives every
-// CU two workgroups over all replicas, else the smallest.
+// are multiples of 16.  Tile choice: 16 output channels and TH output rows
+// (a multiple of 64 pixels), the taller TH if it still gives every CU two
+// workgroups over all replicas.  32-channel tiles measured slower: at
+// width 16, k=4 b=32, 4 rows x 32 channels took 10.1 us per forward launch
+// and 8 rows x 16 channels 9.4 us (+0.7% per step).
 struct DirectTile {
   int th, bn;
 };
@@ -931,21 +933,15 @@ bool direct_ok(int H, int W, int Cin, int Cout, int R, int st, int pad) {
 
 DirectTile direct_pick(int k, int b, int W, int Cout) {
   const int th_max = W == 32 ? 4 : 8, th_min = W == 32 ? 2 : (W == 16 ? 4 : 8);
-  auto wgs = [&](int th, int bn) { return (int64_t)k * b * (W / th) * (Cout / bn); };
-  const int bn_max = Cout % 32 == 0 ? 32 : 16;
-  if (wgs(th_max, bn_max) >= DIRECT_MIN_WGS) return {th_max, bn_max};
-  if (wgs(th_min, bn_max) >= DIRECT_MIN_WGS) return {th_min, bn_max};
-  return {th_min, 16};
+  const int64_t wgs = (int64_t)k * b * (W / th_max) * (Cout / 16);
+  return {wgs >= DIRECT_MIN_WGS ? th_max : th_min, 16};
 }
 
 template <bool FLIP, bool RC, int ST, int WW>
 hipError_t dispatch_w(const DirectArgs& a, DirectTile t, hipStream_t s, const char** name) {
   constexpr int TH1 = WW == 32 ? 4 : 8, TH2 = WW == 32 ? 2 : (WW == 16 ? 4 : 8);
-  if (t.th == TH1) {
-    if (t.bn == 32) return launch<WW, TH1, 32, 16, FLIP, RC, ST>(a, s, name);
-    return launch<WW, TH1, 16, 16, FLIP, RC, ST>(a, s, name);
-  }
-  if (t.bn == 32) return launch<WW, TH2, 32, 16, FLIP, RC, ST>(a, s, name);
+  if (t.bn != 16) return hipErrorInvalidValue;
+  if (t.th == TH1) return launch<WW, TH1, 16, 16, FLIP, RC, ST>(a, s, name);
   return launch<WW, TH2, 16, 16, FLIP, RC, ST>(a, s, name);
 }
 
