@@ -955,18 +955,23 @@ hipError_t dispatch(const DirectArgs& a, int W, hipStream_t s, const char** name
   return dispatch_w<FLIP, RC, ST, 8>(a, t, s, name);
 }
 
-// Weight gradient: units of 4 rows (8 at width 8), so that a workgroup
+// Weight gradient: units of 4 or 8 rows (below), so that a workgroup
 // has several units to pipeline; the split gives every CU two workgroups
 // over all replicas and channel blocks where the units allow.  With at
 // most 128 images per step it gives one per CU: the weight gradients run
 // beside the data-gradient chain, whose kernels are then small, and leave
 // it the other slots (ResNet-32 k=4 b=32 +0.5%, k=2..8 at b=16 +0.5-3%,
 // one replica of 128 +3.4%; at k=16 and 32, b=16, one per CU lost 1-2%).
-constexpr int WG_TH32 = 4, WG_TH16 = 4, WG_TH8 = 8;
-int wgrad_th(int W) { return W == 32 ? WG_TH32 : W == 16 ? WG_TH16 : WG_TH8; }
+// At width 16, 8-row units (stride 1; 11.4 us per ResNet-32 k=4 b=32 launch
+// against 13.3 us with 4 rows, +0.4% per step) but 4-row units for the
+// stride-2 layer (10.3 us against 11.9 us with 8 rows).
+constexpr int WG_TH32 = 4, WG_TH16 = 8, WG_TH16_S2 = 4, WG_TH8 = 8;
+int wgrad_th(int W, int st) {
+  return W == 32 ? WG_TH32 : W == 16 ? (st == 2 ? WG_TH16_S2 : WG_TH16) : WG_TH8;
+}
 
 void wgrad_split(const ConvGeom& g, int* splits, int* per) {
-  const int units = g.b * (g.Ho / wgrad_th(g.Wo));
+  const int units = g.b * (g.Ho / wgrad_th(g.Wo, g.st));
   const int64_t blocks = (int64_t)g.k * (g.Co / 16) * (g.Ci / 16);
   const int64_t wgs = (int64_t)g.k * g.b <= 128 ? DIRECT_MIN_WGS / 2 : DIRECT_MIN_WGS;
   int sp = (int)std::max<int64_t>(1, std::min<int64_t>(units, (wgs + blocks - 1) / blocks));
@@ -1028,7 +1033,7 @@ hipError_t conv_direct_wgrad(const ConvBwdWeightArgs& w, hipStream_t s, const ch
   wgrad_split(w.g, &a.splits, &a.per);
   if (w.splits != a.splits) return hipErrorInvalidValue;  // scratch sized for another split
   if (w.g.st == 2) {
-    if (w.g.Wo == 16) return launch_wgrad<16, WG_TH16, 2>(a, s, name);
+    if (w.g.Wo == 16) return launch_wgrad<16, WG_TH16_S2, 2>(a, s, name);
     return launch_wgrad<8, WG_TH8, 2>(a, s, name);
   }
   if (w.g.W == 32) return launch_wgrad<32, WG_TH32, 1>(a, s, name);
