@@ -962,6 +962,8 @@ hipError_t dispatch(const DirectArgs& a, int W, hipStream_t s, const char** name
 // beside the data-gradient chain, whose kernels are then small, and leave
 // it the other slots (ResNet-32 k=4 b=32 +0.5%, k=2..8 at b=16 +0.5-3%,
 // one replica of 128 +3.4%; at k=16 and 32, b=16, one per CU lost 1-2%).
+// The 32x32 layers keep two per CU (k=4 b=32 +0.5%; two per CU for the
+// 16x16 or the 8x8 layers instead measured -0.1% and -0.6%).
 // At width 16, 8-row units (stride 1; 11.4 us per ResNet-32 k=4 b=32 launch
 // against 13.3 us with 4 rows, +0.4% per step) but 4-row units for the
 // stride-2 layer (10.3 us against 11.9 us with 8 rows).
@@ -973,7 +975,8 @@ int wgrad_th(int W, int st) {
 void wgrad_split(const ConvGeom& g, int* splits, int* per) {
   const int units = g.b * (g.Ho / wgrad_th(g.Wo, g.st));
   const int64_t blocks = (int64_t)g.k * (g.Co / 16) * (g.Ci / 16);
-  const int64_t wgs = (int64_t)g.k * g.b <= 128 ? DIRECT_MIN_WGS / 2 : DIRECT_MIN_WGS;
+  const int64_t wgs =
+      ((int64_t)g.k * g.b <= 128 && g.Wo != 32) ? DIRECT_MIN_WGS / 2 : DIRECT_MIN_WGS;
   int sp = (int)std::max<int64_t>(1, std::min<int64_t>(units, (wgs + blocks - 1) / blocks));
   const int pr = (units + sp - 1) / sp;
   *per = pr;
