@@ -58,6 +58,10 @@ def lib():
         L.cbref_tensor_info.argtypes = [_P, ctypes.c_int, _P, _P, _P, _P]
         L.cbref_learner_grad.argtypes = [_P, _P, _P, _P, ctypes.c_int, _P, _P]
         L.cbref_learner_margin.argtypes = [_P, _P, _P, _P, ctypes.c_int, _P, _P]
+        L.cbref_learner_decisions.argtypes = [_P, _P, _P, _P, ctypes.c_int, ctypes.c_double,
+                                              ctypes.c_int, _P, _P, _P, _P, _P]
+        L.cbref_learner_grad_flipped.argtypes = [_P, _P, _P, _P, ctypes.c_int, ctypes.c_int,
+                                                 _P, _P, _P, _P, _P]
         L.cbref_create.restype = _P
         L.cbref_create.argtypes = [_P, _P, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_double, ctypes.c_double, ctypes.c_double,
@@ -155,6 +159,60 @@ def learner_margin(m: Model, w, x, y, with_bn=False):
     if rc:
         raise ValueError("cbref_learner_margin failed")
     return (out.value, cond.value) if with_bn else out.value
+
+
+DECISION_DTYPE = np.dtype([("site", np.int32), ("idx", np.int64), ("alt", np.int64),
+                           ("rel", np.float64)])
+
+
+def learner_decisions(m: Model, w, x, y, delta: float):
+    """Decisions of one learner's forward pass that lie within delta (relative
+    to the layer's RMS) of turning the other way: a structured array with
+    fields site (ReLU or max pool, numbered in forward order), idx (element
+    or pooled output), alt (runner-up cell of a max-pool window, -1 for a
+    ReLU) and rel (the relative margin), in forward order."""
+    w = _f64(w)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    cap = 256
+    while True:
+        site = np.empty(cap, np.int32)
+        idx = np.empty(cap, np.int64)
+        alt = np.empty(cap, np.int64)
+        rel = np.empty(cap, np.float64)
+        count = ctypes.c_int()
+        rc = lib().cbref_learner_decisions(ctypes.byref(m), _ptr(w), _ptr(x), _ptr(y), len(y),
+                                           float(delta), cap, _ptr(site), _ptr(idx), _ptr(alt),
+                                           _ptr(rel), ctypes.byref(count))
+        if rc:
+            raise ValueError("cbref_learner_decisions failed")
+        if count.value <= cap:
+            break
+        cap = count.value
+    n = count.value
+    out = np.empty(n, DECISION_DTYPE)
+    out["site"], out["idx"], out["alt"], out["rel"] = site[:n], idx[:n], alt[:n], rel[:n]
+    return out
+
+
+def learner_grad_flipped(m: Model, w, x, y, flips):
+    """Mean loss and gradient of one learner's batch with the given decisions
+    (rows of learner_decisions' array) taken the other way."""
+    w = _f64(w)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    flips = np.asarray(flips, dtype=DECISION_DTYPE).reshape(-1)
+    site = np.ascontiguousarray(flips["site"], dtype=np.int32)
+    idx = np.ascontiguousarray(flips["idx"], dtype=np.int64)
+    alt = np.ascontiguousarray(flips["alt"], dtype=np.int64)
+    g = np.empty_like(w)
+    loss = ctypes.c_double()
+    rc = lib().cbref_learner_grad_flipped(ctypes.byref(m), _ptr(w), _ptr(x), _ptr(y), len(y),
+                                          len(flips), _ptr(site), _ptr(idx), _ptr(alt), _ptr(g),
+                                          ctypes.byref(loss))
+    if rc:
+        raise ValueError("cbref_learner_grad_flipped failed")
+    return loss.value, g
 
 
 class SMA:

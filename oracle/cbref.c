@@ -255,11 +255,67 @@ static int build_net(const cbref_model* m, Net* n) {
  * any value on which a ReLU or a max-pool decision turns.  A decision whose
  * margin is within rounding can go either way in another precision; the
  * tests use this to know which inputs make every decision unambiguous.
- * Single-threaded oracle: one running minimum, reset by the API. */
-static double g_margin = INFINITY;
+ * Each computation is single-threaded; the running minimum (like all the
+ * bookkeeping below) belongs to the calling thread, reset by the API, so
+ * independent calls may run on different threads. */
+static _Thread_local double g_margin = INFINITY;
 
 static void note_margin(double m) {
   if (m < g_margin) g_margin = m;
+}
+
+/* Decisions of one forward pass.  Every ReLU and every max pool is a
+ * "site", numbered in forward order from 0.  A ReLU decision is element
+ * idx of the site's tensor (kept iff its input is positive); a max-pool
+ * decision is output idx of the site (the cell that wins its window).
+ * When a decision's value lies within rounding of the point where it
+ * turns, the other outcome is also a correct result at that precision.
+ * The API can list such decisions (relative margin below delta, with the
+ * runner-up cell as the alternative outcome for a max pool) and can compute
+ * the gradient with chosen decisions taken the other way: the forward pass
+ * is left as computed (the two outcomes differ by less than the margin
+ * there), only the backward pass routes the gradient by the flipped
+ * outcome. */
+#define MAX_SITES 256
+
+typedef struct {
+  int nsites;
+  const void* site_key[MAX_SITES]; /* ReLU: its output tensor; max pool: its winners */
+  /* listing (delta > 0) */
+  double delta;
+  int cap, count;
+  int* d_site;
+  int64_t *d_idx, *d_alt;
+  double* d_rel;
+  /* decisions taken the other way */
+  int nflip;
+  const int* f_site;
+  const int64_t *f_idx, *f_alt;
+} Decisions;
+
+static _Thread_local Decisions g_dec;
+
+static int new_site(const void* key) {
+  if (g_dec.nsites >= MAX_SITES) return -1;
+  g_dec.site_key[g_dec.nsites] = key;
+  return g_dec.nsites++;
+}
+
+static int find_site(const void* key) {
+  for (int s = g_dec.nsites - 1; s >= 0; --s)
+    if (g_dec.site_key[s] == key) return s;
+  return -1;
+}
+
+static void note_decision(int site, int64_t idx, int64_t alt, double rel) {
+  if (site < 0 || !(rel < g_dec.delta)) return;
+  if (g_dec.count < g_dec.cap) {
+    g_dec.d_site[g_dec.count] = site;
+    g_dec.d_idx[g_dec.count] = idx;
+    g_dec.d_alt[g_dec.count] = alt;
+    g_dec.d_rel[g_dec.count] = rel;
+  }
+  g_dec.count++;
 }
 
 /* Batch-norm conditioning: the largest, over channels, of
@@ -267,7 +323,7 @@ static void note_margin(double m) {
  * error in the norm's input grows in its output.  Over very few values a
  * channel can have a spread far below its mean, and then fp32 inputs carry
  * little of the normalised output's precision. */
-static double g_bn_cond = 0.0;
+static _Thread_local double g_bn_cond = 0.0;
 
 static double* dalloc(size_t n) {
   double* p = (double*)calloc(n ? n : 1, sizeof(double));
@@ -486,20 +542,44 @@ static void bn_bwd(const BN* b, const double* w, const double* x, int N, int HW,
 
 
 static void relu_inplace(double* y, size_t n) {
+  const int site = new_site(y);
   double ss = 0.0, mn = INFINITY;
   for (size_t i = 0; i < n; ++i) {
     ss += y[i] * y[i];
     if (fabs(y[i]) < mn) mn = fabs(y[i]);
   }
-  if (n && ss > 0.0) note_margin(mn / sqrt(ss / n));
+  if (n && ss > 0.0) {
+    const double rms = sqrt(ss / n);
+    note_margin(mn / rms);
+    if (g_dec.delta > 0.0)
+      for (size_t i = 0; i < n; ++i) note_decision(site, (int64_t)i, -1, fabs(y[i]) / rms);
+  }
   for (size_t i = 0; i < n; ++i)
     if (!(y[i] > 0.0)) y[i] = 0.0;
 }
 
-/* dy <- dy where the layer's output was positive, else 0 (ReLU'(0) = 0). */
+/* dy <- dy where the layer's output was positive, else 0 (ReLU'(0) = 0);
+ * a decision listed to be taken the other way keeps dy where the output is
+ * 0 and zeroes it where the output is positive. */
 static void relu_mask(double* dy, const double* out, size_t n) {
+  const int site = g_dec.nflip ? find_site(out) : -1;
+  double* keep = NULL;
+  if (site >= 0) {
+    keep = dalloc((size_t)g_dec.nflip);
+    for (int f = 0; f < g_dec.nflip; ++f)
+      if (g_dec.f_site[f] == site && g_dec.f_idx[f] >= 0 && (size_t)g_dec.f_idx[f] < n)
+        keep[f] = dy[g_dec.f_idx[f]];
+  }
   for (size_t i = 0; i < n; ++i)
     if (!(out[i] > 0.0)) dy[i] = 0.0;
+  if (site >= 0) {
+    for (int f = 0; f < g_dec.nflip; ++f)
+      if (g_dec.f_site[f] == site && g_dec.f_idx[f] >= 0 && (size_t)g_dec.f_idx[f] < n) {
+        const int64_t i = g_dec.f_idx[f];
+        dy[i] = out[i] > 0.0 ? 0.0 : keep[f];
+      }
+    free(keep);
+  }
 }
 
 /* Max pool K x K, stride st, padding pad.  The winner of a window is the
@@ -507,8 +587,10 @@ static void relu_mask(double* dy, const double* out, size_t n) {
  * greater than every earlier one; padded cells never win. */
 static void maxpool_fwd(const double* x, int N, int C, int H, int W, int K, int st, int pad,
                         double* y, int Ho, int Wo, int* arg) {
+  const int site = new_site(arg);
   double ss = 0.0, gap = INFINITY;
   for (size_t i = 0; i < (size_t)N * C * H * W; ++i) ss += x[i] * x[i];
+  const double rms = ss > 0.0 ? sqrt(ss / ((double)N * C * H * W)) : 0.0;
   for (size_t nc = 0; nc < (size_t)N * C; ++nc)
     for (int oh = 0; oh < Ho; ++oh)
       for (int ow = 0; ow < Wo; ++ow) {
@@ -535,10 +617,21 @@ static void maxpool_fwd(const double* x, int N, int C, int H, int W, int K, int 
               if (ih < 0 || ih >= H || iw < 0 || iw >= W || ih * W + iw == best) continue;
               double d = x[nc * H * W + best] - x[nc * H * W + ih * W + iw];
               if (d < gap) gap = d;
+              if (g_dec.delta > 0.0 && rms > 0.0)
+                note_decision(site, (int64_t)(nc * Ho * Wo + oh * Wo + ow), ih * W + iw,
+                              d / rms);
             }
       }
   size_t n = (size_t)N * C * H * W;
   if (n && ss > 0.0 && gap < INFINITY) note_margin(gap / sqrt(ss / n));
+  /* windows whose winner is to be taken the other way: the gradient goes
+   * to the alternative cell, the forward value stays */
+  if (site >= 0)
+    for (int f = 0; f < g_dec.nflip; ++f)
+      if (g_dec.f_site[f] == site && g_dec.f_idx[f] >= 0 &&
+          g_dec.f_idx[f] < (int64_t)N * C * Ho * Wo && g_dec.f_alt[f] >= 0 &&
+          g_dec.f_alt[f] < (int64_t)H * W)
+        arg[g_dec.f_idx[f]] = (int)g_dec.f_alt[f];
 }
 
 static void maxpool_bwd(const double* dy, const int* arg, int N, int C, int H, int W, int Ho,
@@ -861,6 +954,7 @@ static double resnet50_grad(const Net* net, const double* w, const double* x, co
 
 static double net_grad(const Net* net, const double* w, const double* x, const int32_t* y,
                        int N, double* g) {
+  g_dec.nsites = 0;
   switch (net->m.arch) {
     case CBREF_ARCH_LENET5: return lenet_grad(net, w, x, y, N, g);
     case CBREF_ARCH_RESNET32: return resnet32_grad(net, w, x, y, N, g);
@@ -938,6 +1032,49 @@ int cbref_learner_margin(const cbref_model* m, const double* w, const float* x,
   int rc = cbref_learner_grad(m, w, x, y, N, NULL, &loss);
   *margin = g_margin;
   if (bn_cond) *bn_cond = g_bn_cond;
+  return rc;
+}
+
+/* The decisions of the forward pass of one learner's batch whose relative
+ * margin is below delta (see Decisions above): for each, its site, its
+ * index, the alternative outcome (the runner-up cell of a max-pool window,
+ * -1 for a ReLU) and its relative margin, in the order the forward pass
+ * meets them.  At most cap are written; *count receives how many there
+ * are.  Returns 0, or -1 on a bad model, label or argument. */
+int cbref_learner_decisions(const cbref_model* m, const double* w, const float* x,
+                            const int32_t* y, int N, double delta, int cap, int* site,
+                            int64_t* idx, int64_t* alt, double* rel, int* count) {
+  if (!(delta > 0.0) || cap < 0 || (cap > 0 && (!site || !idx || !alt || !rel))) return -1;
+  double loss;
+  memset(&g_dec, 0, sizeof(g_dec));
+  g_dec.delta = delta;
+  g_dec.cap = cap;
+  g_dec.d_site = site;
+  g_dec.d_idx = idx;
+  g_dec.d_alt = alt;
+  g_dec.d_rel = rel;
+  int rc = cbref_learner_grad(m, w, x, y, N, NULL, &loss);
+  *count = g_dec.count;
+  memset(&g_dec, 0, sizeof(g_dec));
+  return rc;
+}
+
+/* Loss and gradient of one learner's batch (as cbref_learner_grad) with
+ * the nflip listed decisions taken the other way in the backward pass:
+ * site[i], idx[i] and alt[i] as cbref_learner_decisions reports them.
+ * Returns 0, or -1 on a bad model or label. */
+int cbref_learner_grad_flipped(const cbref_model* m, const double* w, const float* x,
+                               const int32_t* y, int N, int nflip, const int* site,
+                               const int64_t* idx, const int64_t* alt, double* g,
+                               double* loss) {
+  if (nflip < 0 || (nflip > 0 && (!site || !idx || !alt))) return -1;
+  memset(&g_dec, 0, sizeof(g_dec));
+  g_dec.nflip = nflip;
+  g_dec.f_site = site;
+  g_dec.f_idx = idx;
+  g_dec.f_alt = alt;
+  int rc = cbref_learner_grad(m, w, x, y, N, g, loss);
+  memset(&g_dec, 0, sizeof(g_dec));
   return rc;
 }
 
