@@ -38,6 +38,12 @@
 extern "C" {
 #endif
 
+/* Version of this interface: raised with every change to a declaration
+ * below.  cb_abi_version() returns the value the library was built with;
+ * a caller built against another version must not call anything else. */
+#define CB_ABI_VERSION 2
+int cb_abi_version(void);
+
 typedef struct cb_ctx cb_ctx;
 
 enum {
@@ -144,6 +150,13 @@ int cb_get_loss(cb_ctx* c, float* out_host);
  * update as cb_sync; any gradient pending from cb_step is discarded. */
 int cb_sma_apply(cb_ctx* c, const float* grads_dev);
 
+/* A local step with gradients supplied by the caller (the update of a
+ * cb_step whose gradient was never synchronised, i.e. a sync interval above
+ * one): w_j <- w_j - lr g_j (+ mu_L (w_j - w_j_prev)) for every learner,
+ * with no correction; z and z_prev are untouched.  grads_dev as for
+ * cb_sma_apply; any gradient pending from cb_step is discarded. */
+int cb_local_apply(cb_ctx* c, const float* grads_dev);
+
 /* Overwrites the state from host arrays: W [k][P] replicas, z, z_prev [P];
  * w_prev (learner momentum only) is set equal to W.  Clears any pending
  * gradient.  Blocks until the copies are done. */
@@ -212,15 +225,25 @@ int cb_tuner_next(int l, double t, double t_prev, double threshold, int l_max);
 size_t cb_test_conv_scratch_bytes(int k, int b, int Ci, int H, int W, int Co, int R, int stride,
                                   int pad);
 
+/* Number of partial sums per (replica, channel) that the forward epilogue
+ * writes to cb_test_conv's stats; CB_EINVAL on a bad shape. */
+int cb_test_conv_fwd_parts(int k, int b, int Ci, int H, int W, int Co, int R, int stride,
+                           int pad);
+
 /* Convolution or FC (a 1x1 conv on 1x1 images), Sec. 2.1 forward pass:
  * y = conv(x, w) + bias, then ReLU if relu.  x [k*b][Ci][H][W],
- * y [k*b][Co][Ho][Wo].  If dy is not NULL, also the backward pass: the
+ * y [k*b][Co][Ho][Wo].  If stats is not NULL, the forward epilogue also
+ * writes the per-channel partial sums of the stored y that a following
+ * batch norm takes its statistics from, as cb_step uses them:
+ * stats [k][Co][parts][2] (fp64; sum of y, sum of y*y; parts =
+ * cb_test_conv_fwd_parts()), whose sum over parts is the total over the
+ * replica's b images.  If dy is not NULL, also the backward pass: the
  * weight (and bias) gradient into grads and, if dx is not NULL, the input
  * gradient (dy is taken as already masked by any ReLU). */
 int cb_test_conv(int k, int b, int Ci, int H, int W, int Co, int R, int stride, int pad,
                  int relu, int has_bias, const float* x, const float* params, int64_t pstride,
-                 float* y, const float* dy, float* dx, float* grads, void* scratch,
-                 size_t scratch_bytes, void* stream);
+                 float* y, double* stats, const float* dy, float* dx, float* grads,
+                 void* scratch, size_t scratch_bytes, void* stream);
 
 /* Scratch for the batch-norm hooks; 0 on bad shape. */
 size_t cb_test_bn_scratch_bytes(int k, int b, int C, int H, int W);
@@ -275,6 +298,28 @@ int cb_test_conv_dgrad(int k, int b, int Ci, int H, int W, int Co, int R, int st
                        int add_C, const float* bn_x, const float* bn_y, const float* bn_mean,
                        const float* bn_istd, const float* bn_gamma, double* bn_part,
                        void* stream);
+
+/* 1 if the fused network head takes C channels of H x W pixels and
+ * `classes` outputs, else 0. */
+int cb_test_head_ok(int C, int H, int W, int classes);
+
+/* The fused head of the ResNet workloads as cb_step runs it: global average
+ * pool of y [k*b][C][H][W] into features [k*b][C], an FC layer (weights
+ * [classes][C] then bias at params + j*pstride), softmax cross-entropy
+ * (Eq. 2) with per-image loss terms loss [k*b] (a replica's loss is the
+ * mean of its b terms) and logit gradients dlogits [k*b][classes]
+ * (softmax - onehot)/b, then the backward pass down to the pooled input:
+ * dy [k*b][C][H][W].  If bn_part is not NULL, y is the output of a batch
+ * norm with input bn_x and statistics bn_mean / bn_istd [k][C] (ReLU'd if
+ * bn_relu): with d = dy where y > 0 (all of dy without the ReLU) and
+ * xh = (bn_x - mean) * istd, the per-image sums of d and d*xh per replica
+ * and channel go to bn_part [k][C][b][2] (fp64).  Device pointers 16-byte
+ * aligned; CB_EINVAL for a shape cb_test_head_ok rejects. */
+int cb_test_head(int k, int b, int C, int H, int W, int classes, const float* y,
+                 const float* params, int64_t pstride, const int32_t* labels, float* features,
+                 float* dlogits, float* loss, float* dy, const float* bn_x,
+                 const float* bn_mean, const float* bn_istd, int bn_relu, double* bn_part,
+                 void* stream);
 
 /* Mean softmax cross-entropy of each replica's b rows of logits (Eq. 2),
  * loss [k], and its gradient dlogits [k*b][classes]. */

@@ -61,6 +61,7 @@
  *     [out][in] then bias.  In a ResNet-50 block the projection shortcut
  *     comes after the main path.
  */
+#include <float.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -272,10 +273,11 @@ static void note_margin(double m) {
  * turns, the other outcome is also a correct result at that precision.
  * The API can list such decisions (relative margin below delta, with the
  * runner-up cell as the alternative outcome for a max pool) and can compute
- * the gradient with chosen decisions taken the other way: the forward pass
- * is left as computed (the two outcomes differ by less than the margin
- * there), only the backward pass routes the gradient by the flipped
- * outcome. */
+ * the gradient with chosen decisions taken the other way.  A flipped ReLU
+ * outputs 0, or the magnitude of its input, instead of its usual output (a
+ * change within the margin), so that later decisions see the flip; a
+ * flipped max pool keeps its forward value (the two cells differ by less
+ * than the margin) and routes the gradient to the alternative cell. */
 #define MAX_SITES 256
 
 typedef struct {
@@ -541,6 +543,11 @@ static void bn_bwd(const BN* b, const double* w, const double* x, int N, int HW,
 
 
 
+/* In place: y <- max(y, 0).  A decision listed to be taken the other way
+ * outputs 0 where the input is positive, and the input's magnitude (a
+ * positive value within the margin of 0) where it is not, so that the
+ * decisions downstream see it -- a max pool over ReLU outputs then lets
+ * that cell win a window of zeros, as the other precision does. */
 static void relu_inplace(double* y, size_t n) {
   const int site = new_site(y);
   double ss = 0.0, mn = INFINITY;
@@ -554,32 +561,29 @@ static void relu_inplace(double* y, size_t n) {
     if (g_dec.delta > 0.0)
       for (size_t i = 0; i < n; ++i) note_decision(site, (int64_t)i, -1, fabs(y[i]) / rms);
   }
-  for (size_t i = 0; i < n; ++i)
-    if (!(y[i] > 0.0)) y[i] = 0.0;
-}
-
-/* dy <- dy where the layer's output was positive, else 0 (ReLU'(0) = 0);
- * a decision listed to be taken the other way keeps dy where the output is
- * 0 and zeroes it where the output is positive. */
-static void relu_mask(double* dy, const double* out, size_t n) {
-  const int site = g_dec.nflip ? find_site(out) : -1;
-  double* keep = NULL;
-  if (site >= 0) {
-    keep = dalloc((size_t)g_dec.nflip);
-    for (int f = 0; f < g_dec.nflip; ++f)
-      if (g_dec.f_site[f] == site && g_dec.f_idx[f] >= 0 && (size_t)g_dec.f_idx[f] < n)
-        keep[f] = dy[g_dec.f_idx[f]];
-  }
-  for (size_t i = 0; i < n; ++i)
-    if (!(out[i] > 0.0)) dy[i] = 0.0;
-  if (site >= 0) {
+  double* flipped = NULL;
+  if (site >= 0 && g_dec.nflip) {
+    flipped = dalloc((size_t)g_dec.nflip);
     for (int f = 0; f < g_dec.nflip; ++f)
       if (g_dec.f_site[f] == site && g_dec.f_idx[f] >= 0 && (size_t)g_dec.f_idx[f] < n) {
-        const int64_t i = g_dec.f_idx[f];
-        dy[i] = out[i] > 0.0 ? 0.0 : keep[f];
+        const double v = y[g_dec.f_idx[f]];
+        flipped[f] = v > 0.0 ? 0.0 : (-v > 0.0 ? -v : DBL_MIN);
       }
-    free(keep);
   }
+  for (size_t i = 0; i < n; ++i)
+    if (!(y[i] > 0.0)) y[i] = 0.0;
+  if (flipped) {
+    for (int f = 0; f < g_dec.nflip; ++f)
+      if (g_dec.f_site[f] == site && g_dec.f_idx[f] >= 0 && (size_t)g_dec.f_idx[f] < n)
+        y[g_dec.f_idx[f]] = flipped[f];
+    free(flipped);
+  }
+}
+
+/* dy <- dy where the layer's output was positive, else 0 (ReLU'(0) = 0). */
+static void relu_mask(double* dy, const double* out, size_t n) {
+  for (size_t i = 0; i < n; ++i)
+    if (!(out[i] > 0.0)) dy[i] = 0.0;
 }
 
 /* Max pool K x K, stride st, padding pad.  The winner of a window is the

@@ -25,9 +25,14 @@ CB_OK, CB_EINVAL, CB_ENOMEM, CB_EDEVICE, CB_ESTATE, CB_ENONFINITE = 0, -1, -2, -
 ARCH = {"lenet5": 1, "resnet32": 2, "resnet50": 3}
 KIND_NAMES = {0: "conv_w", 1: "bias", 2: "bn_gamma", 3: "bn_beta", 4: "fc_w"}
 
+# The interface version these bindings are written for (CB_ABI_VERSION in
+# include/crossbow_sma.h); a library built from other sources is refused.
+ABI_VERSION = 2
+
 # every symbol the header declares
 EXPORTS = (
-    "cb_num_params", "cb_num_tensors", "cb_tensor_info", "cb_workspace_bytes", "cb_create",
+    "cb_abi_version", "cb_local_apply", "cb_test_conv_fwd_parts", "cb_test_head_ok",
+    "cb_test_head", "cb_num_params", "cb_num_tensors", "cb_tensor_info", "cb_workspace_bytes", "cb_create",
     "cb_step", "cb_sync", "cb_wait", "cb_get_central", "cb_get_replica", "cb_get_prev_central",
     "cb_get_grad", "cb_get_loss", "cb_sma_apply", "cb_set_state", "cb_last_error", "cb_destroy",
     "cb_profile_enable", "cb_profile_collect", "cb_profile_entry", "cb_profile_clear",
@@ -54,14 +59,31 @@ _lib = None
 _P = ctypes.c_void_p
 
 
+def check_abi(L, path):
+    """Raises ImportError unless the loaded library L reports ABI_VERSION."""
+    try:
+        fn = L.cb_abi_version
+    except AttributeError:
+        raise ImportError(f"{path} predates interface version {ABI_VERSION} (no cb_abi_version): "
+                          "rebuild it with `python -m paper_1901_02244_amd.build`") from None
+    fn.restype = ctypes.c_int
+    fn.argtypes = []
+    v = fn()
+    if v != ABI_VERSION:
+        raise ImportError(f"{path} implements interface version {v}, these bindings version "
+                          f"{ABI_VERSION}: rebuild it with `python -m paper_1901_02244_amd.build`")
+
+
 def lib():
-    """The loaded library; raises if it is missing (build it first)."""
+    """The loaded library; raises if it is missing (build it first) or was
+    built from other sources than these bindings."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_1901_02244_amd.build` "
                               "(there is no CPU fallback)")
         L = ctypes.CDLL(LIB_PATH)
+        check_abi(L, LIB_PATH)
         L.cb_num_params.restype = ctypes.c_int64
         L.cb_num_params.argtypes = [_P]
         L.cb_num_tensors.argtypes = [_P]
@@ -79,6 +101,7 @@ def lib():
             getattr(L, n).argtypes = [_P, ctypes.c_int, _P, ctypes.c_int64]
         L.cb_get_loss.argtypes = [_P, _P]
         L.cb_sma_apply.argtypes = [_P, _P]
+        L.cb_local_apply.argtypes = [_P, _P]
         L.cb_set_state.argtypes = [_P, _P, _P, _P]
         L.cb_last_error.restype = ctypes.c_char_p
         L.cb_last_error.argtypes = [_P]
@@ -91,8 +114,12 @@ def lib():
         _i = ctypes.c_int
         L.cb_test_conv_scratch_bytes.restype = ctypes.c_size_t
         L.cb_test_conv_scratch_bytes.argtypes = [_i] * 9
-        L.cb_test_conv.argtypes = [_i] * 11 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P, _P,
+        L.cb_test_conv_fwd_parts.argtypes = [_i] * 9
+        L.cb_test_conv.argtypes = [_i] * 11 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P, _P, _P,
                                                ctypes.c_size_t, _P]
+        L.cb_test_head_ok.argtypes = [_i] * 4
+        L.cb_test_head.argtypes = [_i] * 6 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P,
+                                              _P, _i, _P, _P]
         L.cb_test_bn_scratch_bytes.restype = ctypes.c_size_t
         L.cb_test_bn_scratch_bytes.argtypes = [_i] * 5
         L.cb_test_bn_fwd.argtypes = [_i] * 6 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P,
@@ -260,6 +287,11 @@ class Context:
         """grads: cuda float32 [k][P] contiguous raw gradients."""
         assert grads.is_cuda and grads.is_contiguous() and grads.numel() == self.k * self.P
         return self._check(lib().cb_sma_apply(self._c, grads.data_ptr()), "cb_sma_apply")
+
+    def cb_local_apply(self, grads):
+        """A local step (no correction) with grads: cuda float32 [k][P]."""
+        assert grads.is_cuda and grads.is_contiguous() and grads.numel() == self.k * self.P
+        return self._check(lib().cb_local_apply(self._c, grads.data_ptr()), "cb_local_apply")
 
     # -- instrumentation --------------------------------------------------
     def cb_profile_enable(self, on=True):

@@ -1260,24 +1260,40 @@ int cb_get_loss(cb_ctx* c, float* out_host) {
   return CB_OK;
 }
 
-int cb_sma_apply(cb_ctx* c, const float* grads_dev) {
+int cb_abi_version(void) { return CB_ABI_VERSION; }
+
+}  // extern "C"
+
+namespace {
+
+// The update of Algorithm 1 (correct = 1) or a local step (correct = 0)
+// with caller gradients [k][P].
+int apply_grads(cb_ctx* c, const float* grads_dev, int correct) {
   int rc = enter(c);
   if (rc) return rc;
   if (!grads_dev) return fail(c, CB_EINVAL, "grads is NULL");
   const Plan& p = c->p;
   const bool aligned = p.P % 4 == 0 && reinterpret_cast<uintptr_t>(grads_dev) % 16 == 0;
   if (aligned) {
-    rc = enqueue_sma(c, grads_dev, p.P, 1);
+    rc = enqueue_sma(c, grads_dev, p.P, correct);
   } else {
     CB_HIP(c, hipMemcpy2DAsync(c->G(), (size_t)p.Pp * 4, grads_dev, (size_t)p.P * 4,
                                (size_t)p.P * 4, p.k, hipMemcpyDeviceToDevice, c->stream));
-    rc = enqueue_sma(c, c->G(), p.Pp, 1);
+    rc = enqueue_sma(c, c->G(), p.Pp, correct);
   }
   if (rc) return rc;
   c->pending = false;
-  if (p.m.check_finite) return check_finite(c);
+  if (correct && p.m.check_finite) return check_finite(c);
   return CB_OK;
 }
+
+}  // namespace
+
+extern "C" {
+
+int cb_sma_apply(cb_ctx* c, const float* grads_dev) { return apply_grads(c, grads_dev, 1); }
+
+int cb_local_apply(cb_ctx* c, const float* grads_dev) { return apply_grads(c, grads_dev, 0); }
 
 int cb_set_state(cb_ctx* c, const float* W_host, const float* z_host, const float* zprev_host) {
   int rc = enter(c);

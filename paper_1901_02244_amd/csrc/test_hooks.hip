@@ -45,10 +45,17 @@ size_t cb_test_conv_scratch_bytes(int k, int b, int Ci, int H, int W, int Co, in
   return (size_t)std::max<int64_t>(16, (int64_t)k * splits * Co * Ci * R * R * 4);
 }
 
+int cb_test_conv_fwd_parts(int k, int b, int Ci, int H, int W, int Co, int R, int stride,
+                           int pad) {
+  if (!geom_ok(k, b, Ci, H, W, Co, R, stride, pad) || !conv_supported(R, R, stride, false))
+    return CB_EINVAL;
+  return conv_fwd_tiles_m(make_geom(k, b, Ci, H, W, Co, R, stride, pad));
+}
+
 int cb_test_conv(int k, int b, int Ci, int H, int W, int Co, int R, int stride, int pad,
                  int relu, int has_bias, const float* x, const float* params, int64_t pstride,
-                 float* y, const float* dy, float* dx, float* grads, void* scratch,
-                 size_t scratch_bytes, void* stream) {
+                 float* y, double* stats, const float* dy, float* dx, float* grads,
+                 void* scratch, size_t scratch_bytes, void* stream) {
   if (!geom_ok(k, b, Ci, H, W, Co, R, stride, pad) ||
       !conv_supported(R, R, stride, dx != nullptr) || !x || !params || !y)
     return CB_EINVAL;
@@ -65,7 +72,7 @@ int cb_test_conv(int k, int b, int Ci, int H, int W, int Co, int R, int stride, 
   f.pstride = pstride;
   f.y = y;
   f.relu = relu;
-  f.stats = nullptr;
+  f.stats = stats;
   int rc = rc_of(conv_fwd(f, s));
   if (rc || !dy) return rc;
   if (!grads) return CB_EINVAL;
@@ -221,6 +228,37 @@ int cb_test_maxpool(int N, int C, int H, int W, int K, int stride, int pad, cons
   if (!dx) return CB_EINVAL;
   return rc_of(maxpool_bwd(dy, arg_scratch, x, N, C, H, W, K, stride, pad, Ho, Wo, dx, mask_relu,
                            s));
+}
+
+int cb_test_head_ok(int C, int H, int W, int classes) {
+  return C >= 1 && H >= 1 && W >= 1 && head_ok(C, H * W, classes) ? 1 : 0;
+}
+
+int cb_test_head(int k, int b, int C, int H, int W, int classes, const float* y,
+                 const float* params, int64_t pstride, const int32_t* labels, float* features,
+                 float* dlogits, float* loss, float* dy, const float* bn_x,
+                 const float* bn_mean, const float* bn_istd, int bn_relu, double* bn_part,
+                 void* stream) {
+  if (k < 1 || b < 1 || !cb_test_head_ok(C, H, W, classes) || !y || !params || !labels ||
+      !features || !dlogits || !loss || !dy || (bn_part && (!bn_x || !bn_mean || !bn_istd)))
+    return CB_EINVAL;
+  HeadArgs a;
+  a.k = k; a.b = b; a.C = C; a.HW = H * W; a.classes = classes;
+  a.y = y;
+  a.g = features;
+  a.w = params;
+  a.bias = params + (int64_t)classes * C;
+  a.pstride = pstride;
+  a.labels = labels;
+  a.dlogits = dlogits;
+  a.loss = loss;
+  a.dy = dy;
+  a.bn_part = bn_part;
+  a.bn_relu = bn_relu;
+  a.bn_x = bn_part ? bn_x : nullptr;
+  a.bn_mean = bn_part ? bn_mean : nullptr;
+  a.bn_istd = bn_part ? bn_istd : nullptr;
+  return rc_of(head_fwd_bwd(a, static_cast<hipStream_t>(stream)));
 }
 
 int cb_test_softmax_xent(int k, int b, int classes, const float* logits, const int32_t* labels,

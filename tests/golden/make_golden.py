@@ -10,6 +10,7 @@ Run from the repository root:
     python tests/golden/make_golden.py resnet32_envelope # ~1 h
     python tests/golden/make_golden.py resnet50_sampled  # ~10 min
     python tests/golden/make_golden.py lenet_z1000       # ~5 min
+    python tests/golden/make_golden.py resnet50_envelope [trial]  # ~10 min per trial
 
 Jobs:
   lenet_envelope / resnet32_envelope: how far the oracle drifts from itself
@@ -21,6 +22,11 @@ Jobs:
     iterations of ResNet-32, k = 4 learners of batch 32 (float32 .npy).
   resnet50_sampled: learner 0's loss and sampled gradient entries after one
     forward/backward pass of ResNet-50 on 224x224 images, b = 32.
+  resnet50_envelope: learner 0's gradient of the same ResNet-50 pass with w0
+    perturbed by one part in 1e7 (three independent perturbations), at the
+    sampled entries of resnet50_sampled: how far the oracle's own sampled
+    gradient moves, per tensor, when rounding-sized noise flips the ReLU
+    and max-pool decisions that lie within rounding of turning.
   lenet_z1000: LeNet-5, k = 8 learners of 16, the full 1000 SMA iterations:
     the central model after 1000 (float32 .npy) and the oracle's drift
     from itself (as in the envelope jobs) after 100, 300 and 1000.
@@ -135,6 +141,32 @@ def lenet_z1000():
               open(os.path.join(HERE, "lenet5_k8_b16_z1000.json"), "w"), indent=1)
 
 
+def resnet50_envelope(trial):
+    wk = wl.RESNET50_K2
+    m = oracle.model(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
+    gold = json.load(open(os.path.join(HERE, "resnet50_k2_b32_learner0.json")))
+    w0 = wl.init_w0(oracle.tensors(m), wk.seed)
+    eps = np.random.default_rng(777 + trial).standard_normal(w0.size).astype(np.float32)
+    w0 = (w0 * (1 + PERTURB * eps)).astype(np.float32)
+    x, y = wl.workload_batch(wk, 0)
+    t0 = time.time()
+    loss, g = oracle.learner_grad(m, w0, x[:wk.b], y[:wk.b])
+    rows = []
+    for t in gold["tensors"]:
+        idx = np.array(t["index"])
+        d = g[idx] - np.array(t["value"])
+        rows.append({"offset": t["offset"],
+                     "max_rel": float(np.abs(d).max() / t["max_abs"]),
+                     "rel_l2": float(np.linalg.norm(d) / max(np.linalg.norm(t["value"]), 1e-300))})
+    name = f"resnet50_k2_b32_envelope{trial}.json"
+    json.dump({"workload": wk.name, "learner": 0, "perturbation": PERTURB, "trial": trial,
+               "what": "learner 0's sampled gradient at w0*(1+1e-7*N(0,1)) against the stored "
+                       "one at w0: per tensor max|d|/max|g| and relative L2 over the samples",
+               "loss_rel": abs(loss - gold["loss"]) / gold["loss"],
+               "seconds": round(time.time() - t0), "tensors": rows},
+              open(os.path.join(HERE, name), "w"), indent=0)
+
+
 if __name__ == "__main__":
     job = sys.argv[1]
     if job == "lenet_envelope":
@@ -147,6 +179,8 @@ if __name__ == "__main__":
         resnet32_z(10)
     elif job == "lenet_z1000":
         lenet_z1000()
+    elif job == "resnet50_envelope":
+        resnet50_envelope(int(sys.argv[2]) if len(sys.argv) > 2 else 0)
     elif job == "resnet50_sampled":
         resnet50_sampled()
     else:

@@ -113,3 +113,37 @@ def test_tuner_rule_matches_oracle(oracle_lib):
             assert l_lib == l_ref
             assert 1 <= l_lib <= l_max
             tp = float(t)
+
+
+def test_abi_version_matches_header():
+    src = open(HEADER).read()
+    v = int(re.search(r"#define CB_ABI_VERSION (\d+)", src).group(1))
+    assert cb.ABI_VERSION == v
+    L = cb.lib()
+    L.cb_abi_version.restype = ctypes.c_int
+    assert L.cb_abi_version() == v
+
+
+def _stub(tmp_path, name, body):
+    src = tmp_path / f"{name}.c"
+    so = tmp_path / f"lib{name}.so"  # a distinct path each: dlopen caches by path
+    src.write_text(body)
+    import subprocess
+    subprocess.run(["gcc", "-shared", "-fPIC", str(src), "-o", str(so)], check=True)
+    return ctypes.CDLL(str(so)), str(so)
+
+
+def test_stale_library_is_refused(tmp_path):
+    """A library built from other sources (another interface version, or one
+    from before the version call existed) raises ImportError instead of
+    being called with arguments it does not take."""
+    L, path = _stub(tmp_path, "older", "int cb_abi_version(void) { return %d; }\n" %
+                    (cb.ABI_VERSION - 1))
+    with pytest.raises(ImportError, match="interface version"):
+        cb.check_abi(L, path)
+    L, path = _stub(tmp_path, "unversioned", "int cb_num_params(const void* m) { return -1; }\n")
+    with pytest.raises(ImportError, match="predates"):
+        cb.check_abi(L, path)
+    L, path = _stub(tmp_path, "current", "int cb_abi_version(void) { return %d; }\n" %
+                    cb.ABI_VERSION)
+    cb.check_abi(L, path)

@@ -55,6 +55,8 @@ CONV = [
     # 3x3 stride-1 layers of the direct kernel: every tile choice, bias and
     # ReLU, channel counts that are not multiples of 32, k = 1 and k = 32
     ("direct.w32.k1", 1, 16, 16, 32, 16, 3, 1, 1, 0, 0, 1),
+    ("r32.s1.k2b16", 2, 16, 16, 32, 16, 3, 1, 1, 0, 0, 1),
+    ("r32.s1.k32b16", 32, 16, 16, 32, 16, 3, 1, 1, 0, 0, 1),
     ("direct.w32.bias", 2, 3, 16, 32, 16, 3, 1, 1, 1, 1, 1),
     ("direct.w32.16to32", 2, 4, 16, 32, 32, 3, 1, 1, 1, 0, 1),
     ("direct.w16.c48", 3, 2, 48, 16, 48, 3, 1, 1, 1, 1, 1),
@@ -106,22 +108,36 @@ def test_conv_kernels(case):
     L = cb.lib()
     scratch_n = L.cb_test_conv_scratch_bytes(k, b, Ci, H, W, Co, R, st, pad)
     assert scratch_n > 0
+    # the batch-norm statistics epilogue of every conv that is not an FC layer
+    # (an FC layer with statistics would leave the FC kernel)
+    parts = L.cb_test_conv_fwd_parts(k, b, Ci, H, W, Co, R, st, pad) if H > 1 else 0
     xd, pd, dyd = _dev(x), _dev(params), _dev(dy)
     yd = torch.empty((k * b, Co, Ho, Ho), dtype=torch.float32, device="cuda")
     dxd = torch.empty_like(xd) if need_dx else None
     gd = torch.zeros_like(pd)
     scratch = torch.empty(scratch_n, dtype=torch.uint8, device="cuda")
+    stats = torch.full((max(1, k * Co * parts * 2),), float("nan"), dtype=torch.float64,
+                       device="cuda")
     rc = L.cb_test_conv(k, b, Ci, H, W, Co, R, st, pad, relu, bias, xd.data_ptr(), pd.data_ptr(),
-                        pstride, yd.data_ptr(), dyd.data_ptr(),
+                        pstride, yd.data_ptr(), stats.data_ptr() if parts else None, dyd.data_ptr(),
                         dxd.data_ptr() if need_dx else None, gd.data_ptr(), scratch.data_ptr(),
                         scratch_n, torch.cuda.current_stream().cuda_stream)
     assert rc == 0
     torch.cuda.synchronize()
     y, g = yd.cpu().numpy(), gd.cpu().numpy()
     dx = dxd.cpu().numpy() if need_dx else None
+    # the statistics epilogue: per replica and channel the sums over the
+    # replica's b images of the stored y and of y*y
+    sums = stats.cpu().numpy().reshape(k, Co, parts, 2).sum(axis=2) if parts else None
     macs = b * Ho * Ho * Co * Ci * R * R
     geo = dict(N=b, Ci=Ci, H=H, W=W, Co=Co, R=R, stride=st, pad=pad)
-    for j in sorted({0, k - 1}):
+    if parts and macs > FULL_LIMIT:
+        # too large for the oracle's whole output: the sums must equal those
+        # of the stored y, which is compared with the oracle on samples below
+        yr = y.reshape(k, b, Co, -1).astype(np.float64)
+        assert max_rel(sums[..., 0], yr.sum(axis=(1, 3))) <= TOL_STEP1, (name, "sum y")
+        assert max_rel(sums[..., 1], (yr * yr).sum(axis=(1, 3))) <= TOL_STEP1, (name, "sum y*y")
+    for j in range(k):
         sl = slice(j * b, (j + 1) * b)
         w = params[j * pstride:j * pstride + nw].reshape(Co, Ci, R, R)
         bb = params[j * pstride + nw:j * pstride + nw + Co] if bias else None
@@ -131,6 +147,10 @@ def test_conv_kernels(case):
             if relu:
                 yo = np.maximum(yo, 0.0)
             assert max_rel(y[sl], yo) <= TOL_STEP1, (name, j, "y")
+            if parts:
+                assert max_rel(sums[j, :, 0], yo.sum(axis=(0, 2, 3))) <= TOL_STEP1, (name, j, "sum y")
+                assert max_rel(sums[j, :, 1], (yo * yo).sum(axis=(0, 2, 3))) <= TOL_STEP1, \
+                    (name, j, "sum y*y")
             assert max_rel(gw, dwo) <= TOL_STEP1, (name, j, "dw")
             if bias:
                 assert max_rel(g[j * pstride + nw:j * pstride + nw + Co], dbo) <= TOL_STEP1
@@ -342,6 +362,80 @@ def test_softmax_xent_kernel(case):
         assert max_rel(d[j * b:(j + 1) * b], do) <= TOL_STEP1
 
 
+# (name, k, b, C, H, classes, bn_relu): the ResNet-32 head at the two step
+# sizes of its workloads, and a ragged one
+HEAD = [("r32.k4b32", 4, 32, 64, 8, 10, 1), ("r32.k32b16", 32, 16, 64, 8, 10, 1),
+        ("ragged", 3, 5, 24, 4, 7, 0), ("no_bn", 2, 3, 16, 8, 5, -1)]
+
+
+@pytest.mark.parametrize("case", HEAD, ids=[c[0] for c in HEAD])
+def test_fused_head_kernel(case):
+    """Global average pool, FC, softmax cross-entropy and their backward down
+    to the pooled tensor -- with the backward sums of the batch norm that
+    produced it -- in the one launch cb_step makes, against the oracle's FC
+    (a 1x1 convolution on a 1x1 image) and softmax cross-entropy, with the
+    pool's mean and the norm's masks and sums written out in numpy."""
+    name, k, b, C, H, classes, bn_relu = case
+    HW = H * H
+    L = cb.lib()
+    assert L.cb_test_head_ok(C, H, H, classes) == 1
+    rng = _rng("head" + name)
+    N = k * b
+    bn_x = rng.standard_normal((N, C, H, H), dtype=np.float32)
+    mean = (rng.standard_normal((k, C)) * 0.1).astype(np.float32)
+    istd = rng.uniform(0.5, 2.0, (k, C)).astype(np.float32)
+    y = rng.standard_normal((N, C, H, H), dtype=np.float32)
+    if bn_relu == 1:
+        y = np.maximum(y, 0.0)
+    pstride = classes * C + classes + 3
+    params = np.zeros(k * pstride, dtype=np.float32)
+    for j in range(k):
+        params[j * pstride:j * pstride + classes * C] = rng.standard_normal(classes * C) / np.sqrt(C)
+        params[j * pstride + classes * C:j * pstride + classes * C + classes] = \
+            rng.standard_normal(classes) * 0.1
+    labels = rng.integers(0, classes, N).astype(np.int32)
+    use_bn = bn_relu >= 0
+    d = {n_: _dev(v) for n_, v in dict(y=y, p=params, l=labels, x=bn_x, m=mean, i=istd).items()}
+    feat = torch.empty((N, C), dtype=torch.float32, device="cuda")
+    dlog = torch.empty((N, classes), dtype=torch.float32, device="cuda")
+    loss = torch.empty(N, dtype=torch.float32, device="cuda")
+    dy = torch.empty((N, C, H, H), dtype=torch.float32, device="cuda")
+    part = torch.full((k * C * b * 2,), float("nan"), dtype=torch.float64, device="cuda")
+    rc = L.cb_test_head(k, b, C, H, H, classes, d["y"].data_ptr(), d["p"].data_ptr(), pstride,
+                        d["l"].data_ptr(), feat.data_ptr(), dlog.data_ptr(), loss.data_ptr(),
+                        dy.data_ptr(), d["x"].data_ptr(), d["m"].data_ptr(), d["i"].data_ptr(),
+                        max(bn_relu, 0), part.data_ptr() if use_bn else None,
+                        torch.cuda.current_stream().cuda_stream)
+    assert rc == 0
+    torch.cuda.synchronize()
+    feat, dlog, loss, dy = (t.cpu().numpy() for t in (feat, dlog, loss, dy))
+    sums = part.cpu().numpy().reshape(k, C, b, 2)
+    for j in range(k):
+        sl = slice(j * b, (j + 1) * b)
+        w = params[j * pstride:j * pstride + classes * C].reshape(classes, C, 1, 1)
+        bias = params[j * pstride + classes * C:j * pstride + classes * C + classes]
+        g = y[sl].astype(np.float64).mean(axis=(2, 3))
+        assert max_rel(feat[sl], g) <= TOL_STEP1, (name, j, "features")
+        logits, _, _, _ = oracle.conv2d(g[:, :, None, None], w, bias, 1, 0)
+        lo, dlo = oracle.softmax_xent(logits[:, :, 0, 0], labels[sl])
+        per_image = [oracle.softmax_xent(logits[i:i + 1, :, 0, 0], labels[sl][i:i + 1])[0]
+                     for i in range(b)]
+        assert max_rel(loss[sl], per_image) <= TOL_STEP1, (name, j, "loss terms")
+        assert abs(loss[sl].astype(np.float64).mean() - lo) / abs(lo) <= TOL_STEP1
+        assert max_rel(dlog[sl], dlo) <= TOL_STEP1, (name, j, "dlogits")
+        _, dg, _, _ = oracle.conv2d(g[:, :, None, None], w, bias, 1, 0,
+                                    dy=dlo[:, :, None, None])
+        dyo = np.broadcast_to(dg / HW, (b, C, H, H))
+        assert max_rel(dy[sl], dyo) <= TOL_STEP1, (name, j, "dy")
+        if use_bn:
+            dd = np.where(y[sl] > 0, dyo, 0.0) if bn_relu else dyo
+            xh = (bn_x[sl].astype(np.float64) - mean[j][None, :, None, None]) * \
+                istd[j][None, :, None, None]
+            assert max_rel(sums[j, :, :, 0].T, dd.sum(axis=(2, 3))) <= TOL_STEP1, (name, j, "sum d")
+            assert max_rel(sums[j, :, :, 1].T, (dd * xh).sum(axis=(2, 3))) <= TOL_STEP1, \
+                (name, j, "sum d*xh")
+
+
 # (name, k, b, Ci, H, Co, R, stride, pad, accumulate, mask, add_mode, add_C, bn, bn_y:
 #  0 none, 1 a y tensor, 2 a y tensor that gamma and beta recompute from bn_x,
 #  3 no y: the mask is the norm's own ReLU output, recomputed from bn_x by the
@@ -433,7 +527,7 @@ def test_conv_data_gradient_epilogue(case):
     torch.cuda.synchronize()
     got = d["dx"].cpu().numpy()
     sums = part.cpu().numpy().reshape(k, Ci, parts, 2).sum(axis=2) if bn else None
-    for j in sorted({0, k - 1}):
+    for j in range(k):
         sl = slice(j * b, (j + 1) * b)
         w = params[j * pstride:j * pstride + nw].reshape(Co, Ci, R, R)
         _, ref, _, _ = oracle.conv2d(np.zeros((b, Ci, H, H), np.float32), w, None, st, pad,

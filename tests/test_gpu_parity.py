@@ -1,9 +1,19 @@
 """Parity of the HIP path with the CPU oracle, through the C ABI (needs a GPU).
 
 Bars (the method's stated tolerances): per-tensor max relative error
-<= 1e-4 after one step -- applied to every learner's raw gradient, its loss,
-its replica and z -- and relative L2 of z <= 1e-3 after many steps.
-Inputs are the seeded synthetic workloads of ``workloads``.
+<= 1e-4 after one step -- applied to every learner's loss and raw gradient,
+and to the update each synchronisation makes to every replica and to z --
+and relative L2 of z <= 1e-3 after many steps.  Inputs are the seeded
+synthetic workloads of ``workloads``.
+
+Gradients are compared with parity.resolve_decisions: where a ReLU input or
+a max-pool runner-up lies within rounding of its decision, both outcomes
+are correct, and the GPU's gradient must equal the oracle's under one
+valid set of outcomes, at 1e-4 per tensor.  The oracle then continues from
+the state those outcomes give (its own update of its own state, with its
+own gradients for the chosen outcomes), so later steps and the central
+model after many steps are compared at the stated bars too.  Every
+end-to-end test prints the errors it achieved.
 """
 import json
 import os
@@ -14,8 +24,8 @@ import pytest
 import oracle
 import paper_1901_02244_amd as cb
 import workloads as wl
-from parity import (MARGIN, TOL_AMBIGUOUS, TOL_STEP1, TOL_Z_L2, max_rel, per_tensor_max_rel,
-                    rel_l2)
+from parity import (TOL_STEP1, TOL_Z_L2, describe, displacement_errors, max_rel,
+                    resolve_decisions, tensor_errors)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -30,11 +40,15 @@ def _dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
+def _report(line):
+    print(line, flush=True)
+
+
 class Pair:
     """The same SMA job on the GPU (through the C ABI) and in the oracle."""
 
     def __init__(self, arch, C, H, W, classes, k, b, lr=0.01, mu=0.9, alpha=None, mu_l=0.0,
-                 seed=0):
+                 seed=0, tag=None):
         self.shape = (C, H, W)
         self.classes = classes
         self.m = cb.model(arch, C, H, W, classes, learner_momentum=mu_l)
@@ -45,79 +59,96 @@ class Pair:
         self.gpu = cb.Context(self.m, k, b, alpha, lr, mu, self.w0)
         self.ref = oracle.SMA(oracle.model(arch, C, H, W, classes), self.w0, k, b, f32(alpha),
                               f32(lr), f32(mu), f32(mu_l))
-
         self.om = oracle.model(arch, C, H, W, classes)
+        self.tag = tag or f"{arch} {C}x{H}x{W} k={k} b={b}"
         self.last = None
+        self.t = None
+        self.gres = None       # the oracle's gradients under the GPU's outcomes
+        self.pending = False
+        self.worst = dict(raw=0.0, grad=0.0, loss=0.0, state=0.0, flips=0)
 
     def batch(self, t):
         return wl.batch(self.k * self.b, *self.shape, self.classes, self.seed, t)
 
     def step(self, t):
+        if self.pending and self.gres is not None:
+            raise AssertionError("a local step after resolved decisions: choose inputs whose "
+                                 "unsynchronised steps take no ambiguous decision")
         x, y = self.batch(t)
-        # the oracle's decision margin at the replicas this step starts from
-        # (a pending gradient is applied first, as a local step)
-        self.last = (x, y)
+        self.last, self.t = (x, y), t
         self.gpu.cb_step(_dev(x), _dev(y))
         self.ref.step(x, y)
+        self.gres = None
+        self.pending = True
 
-    def sync(self):
+    def check_grads(self, verbose=True):
+        """Every learner's loss and raw gradient, with ambiguous decisions
+        resolved (see the module docstring)."""
+        x, y = self.last
+        b = self.b
+        lerr = max_rel(self.gpu.cb_get_loss(), self.ref.loss())
+        assert lerr <= TOL_STEP1, ("loss", lerr)
+        self.worst["loss"] = max(self.worst["loss"], lerr)
+        G, flips = [], 0
+        for j in range(self.k):
+            res = resolve_decisions(oracle, self.om, self.ref.replica(j), x[j * b:(j + 1) * b],
+                                    y[j * b:(j + 1) * b], self.gpu.cb_get_grad(j), self.layout,
+                                    g0=self.ref.grad(j))
+            if verbose or res["flips"]:
+                _report(describe(f"{self.tag} step {self.t} learner {j}", res, lerr))
+            if not res["ok"] and os.environ.get("PARITY_DUMP"):
+                # the failing case, for study on the CPU
+                os.makedirs(os.environ["PARITY_DUMP"], exist_ok=True)
+                np.savez(os.path.join(os.environ["PARITY_DUMP"],
+                                      f"{self.tag.replace(' ', '_')}_t{self.t}_j{j}.npz"),
+                         w=self.ref.replica(j), x=x[j * b:(j + 1) * b], y=y[j * b:(j + 1) * b],
+                         g=self.gpu.cb_get_grad(j), w_gpu=self.gpu.cb_get_replica(j))
+            assert res["ok"], (self.tag, self.t, j, {k_: v for k_, v in res.items()
+                                                      if k_ != "resolved"})
+            self.worst["raw"] = max(self.worst["raw"], res["raw_max_rel"])
+            self.worst["grad"] = max(self.worst["grad"], res["err"])
+            self.worst["flips"] += res["flips"]
+            flips += res["flips"]
+            G.append(res["resolved"])
+        self.gres = np.stack(G) if flips else None
+
+    def _gpu_state(self):
+        return [self.gpu.cb_get_replica(j) for j in range(self.k)] + [self.gpu.cb_get_central()]
+
+    def _ref_state(self):
+        return [self.ref.replica(j) for j in range(self.k)] + [self.ref.central()]
+
+    def sync(self, check=True, verbose=False):
+        """One synchronisation on both sides; with check, the update it makes
+        to every replica and to z must agree per tensor at 1e-4."""
+        if check:
+            a0, r0 = self._gpu_state(), self._ref_state()
         self.gpu.cb_sync()
-        assert self.ref.sync() == 0
+        if self.gres is not None:
+            assert self.ref.sma_apply(self.gres) == 0
+        else:
+            assert self.ref.sync() == 0
+        self.gres = None
+        self.pending = False
+        if check:
+            a1, r1 = self._gpu_state(), self._ref_state()
+            errs = [displacement_errors(a0[i], a1[i], r0[i], r1[i], self.layout).max()
+                    for i in range(self.k + 1)]
+            if verbose:
+                _report(f"{self.tag} sync after step {self.t}: update of the replicas "
+                        f"{max(errs[:-1]):.2e}, of z {errs[-1]:.2e} (per-tensor, fp32 slack)")
+            self.worst["state"] = max(self.worst["state"], max(errs))
+            assert max(errs) <= TOL_STEP1, (self.tag, self.t, errs)
 
-    def margin(self, j):
-        """Decision margin of learner j's forward pass at its current replica
-        (the replica the last gradient was taken at when called right after
-        step() with no unsynced gradient before it)."""
-        x, y = self.last
-        b = self.b
-        return oracle.learner_margin(self.om, self.ref.replica(j), x[j * b:(j + 1) * b],
-                                     y[j * b:(j + 1) * b])
+    def z_error(self):
+        return float(np.linalg.norm(self.gpu.cb_get_central() - self.ref.central()) /
+                     np.linalg.norm(self.ref.central()))
 
-    def check_grads(self, tol=TOL_STEP1, require_margin=True):
-        """Every learner's raw gradient per tensor and the losses.  The strict
-        bar needs every ReLU/max-pool decision unambiguous (see parity.MARGIN);
-        with require_margin the test's inputs are chosen so that holds."""
-        assert max_rel(self.gpu.cb_get_loss(), self.ref.loss()) <= TOL_STEP1
-        for j in range(self.k):
-            m = self.margin(j)
-            if require_margin:
-                assert m >= MARGIN, ("inputs chosen for unambiguous decisions", j, m)
-            t = tol if m >= MARGIN else max(tol, TOL_AMBIGUOUS)
-            err, where = per_tensor_max_rel(self.gpu.cb_get_grad(j), self.ref.grad(j), self.layout)
-            assert err <= t, ("grad", j, err, where, "margin", m)
-
-    def check_grads_at_gpu_replicas(self):
-        """Each learner's gradient against the oracle's at the GPU's own
-        replica (after several steps the two trajectories differ by rounding,
-        and a ReLU decision within that distance of zero may go either way).
-        Where the oracle certifies every decision there: per tensor, strict.
-        Otherwise one flipped decision concentrates in one or two tensors
-        (up to 0.11 per tensor at 3 images of 16 x 16, measured on the oracle
-        itself), so the whole gradient vector's relative L2 takes the
-        ambiguity bound; the loss is strict either way."""
-        x, y = self.last
-        b = self.b
-        for j in range(self.k):
-            w = self.gpu.cb_get_replica(j)
-            xj, yj = x[j * b:(j + 1) * b], y[j * b:(j + 1) * b]
-            lj, gj = oracle.learner_grad(self.om, w, xj, yj)
-            m = oracle.learner_margin(self.om, w, xj, yj)
-            assert abs(self.gpu.cb_get_loss()[j] - lj) / abs(lj) <= TOL_STEP1
-            g = self.gpu.cb_get_grad(j)
-            if m >= MARGIN:
-                err, where = per_tensor_max_rel(g, gj, self.layout)
-                assert err <= TOL_STEP1, ("grad", j, err, where, "margin", m)
-            else:
-                err = rel_l2(g, gj)
-                assert err <= TOL_AMBIGUOUS, ("grad rel L2", j, err, "margin", m)
-
-    def check_state(self, tol=TOL_STEP1):
-        for j in range(self.k):
-            err, where = per_tensor_max_rel(self.gpu.cb_get_replica(j), self.ref.replica(j),
-                                            self.layout)
-            assert err <= tol, ("replica", j, err, where)
-        err, where = per_tensor_max_rel(self.gpu.cb_get_central(), self.ref.central(), self.layout)
-        assert err <= tol, ("z", err, where)
+    def summary(self, extra=""):
+        w = self.worst
+        _report(f"{self.tag}: loss {w['loss']:.2e} | gradients raw {w['raw']:.2e} -> resolved "
+                f"{w['grad']:.2e} ({w['flips']} flipped decisions) | updates {w['state']:.2e}"
+                + (f" | {extra}" if extra else ""))
 
 
 # ------------------------------------------------------------- SMA kernel
@@ -128,33 +159,59 @@ MODEL_SHAPES = {"lenet5": (1, 28, 28, 10), "resnet32": (3, 32, 32, 10),
                 "resnet50": (3, 224, 224, 1000)}
 
 
+def _check_update(ctx, k, W0, Z0, Wn, Zn, layout, tag):
+    """Every replica's and z's update against the oracle's, per tensor."""
+    worst = 0.0
+    for j in range(k):
+        e = displacement_errors(W0[j], ctx.cb_get_replica(j), W0[j], Wn[j], layout).max()
+        worst = max(worst, e)
+        assert e <= TOL_STEP1, (tag, "replica", j, e)
+    e = displacement_errors(Z0, ctx.cb_get_central(), Z0, Zn, layout).max()
+    assert e <= TOL_STEP1, (tag, "z", e)
+    return max(worst, e)
+
+
 @pytest.mark.parametrize("arch,k", SMA_CASES)
 @pytest.mark.parametrize("mu_l", [0.0, 0.9])
 def test_sma_kernel_matches_oracle(arch, k, mu_l):
+    """The fused synchronisation on seeded state (every replica and z, per
+    tensor, as updates), then a second one with w_prev != w, then a local
+    step (no correction: z and z_prev bitwise unchanged)."""
     m = cb.model(arch, *MODEL_SHAPES[arch], learner_momentum=mu_l)
     P = cb.cb_num_params(m)
+    layout = cb.cb_tensor_layout(m)
     W, G, Z, Zp = wl.random_state(k, P, seed=100 + k)
     alpha, lr, mu = 1.0 / k, 0.05, 0.9
     ctx = cb.Context(m, k, 1, alpha, lr, mu, Z)
     ctx.cb_set_state(W, Z, Zp)
     ctx.cb_sma_apply(_dev(G))
-    Wn, _, Zn, Zpn = oracle.sma_update(W, G, Z, Zp, f32(alpha), f32(lr), f32(mu), f32(mu_l))
-    for j in range(k):
-        assert max_rel(ctx.cb_get_replica(j), Wn[j]) <= 1e-6
-    assert max_rel(ctx.cb_get_central(), Zn) <= 1e-6
+    Wn, Wp, Zn, Zpn = oracle.sma_update(W, G, Z, Zp, f32(alpha), f32(lr), f32(mu), f32(mu_l))
+    _check_update(ctx, k, W, Z, Wn, Zn, layout, "first")
     np.testing.assert_array_equal(ctx.cb_get_prev_central(), Z)
     # a second application, now with w_prev != w for learner momentum
+    W1 = np.stack([ctx.cb_get_replica(j) for j in range(k)])
+    Z1 = ctx.cb_get_central()
     ctx.cb_sma_apply(_dev(G * 0.5))
-    Wn2, _, Zn2, _ = oracle.sma_update(Wn, G * 0.5, Zn, Zpn, f32(alpha), f32(lr), f32(mu),
-                                       f32(mu_l), Wprev=W)
+    Wn2, Wp2, Zn2, _ = oracle.sma_update(W1, G * 0.5, Z1, Z, f32(alpha), f32(lr), f32(mu),
+                                         f32(mu_l), Wprev=W)
+    _check_update(ctx, k, W1, Z1, Wn2, Zn2, layout, "second")
+    # a local step: replicas only, learner momentum from the previous update
+    W2 = np.stack([ctx.cb_get_replica(j) for j in range(k)])
+    Z2, Zp2 = ctx.cb_get_central(), ctx.cb_get_prev_central()
+    ctx.cb_local_apply(_dev(G * -0.25))
+    Wn3, _, _, _ = oracle.sma_update(W2, G * -0.25, Z2, Zp2, f32(alpha), f32(lr), f32(mu),
+                                     f32(mu_l), Wprev=W1, correct=False)
     for j in range(k):
-        assert max_rel(ctx.cb_get_replica(j), Wn2[j]) <= 1e-5
-    assert max_rel(ctx.cb_get_central(), Zn2) <= 1e-5
+        e = displacement_errors(W2[j], ctx.cb_get_replica(j), W2[j], Wn3[j], layout).max()
+        assert e <= TOL_STEP1, ("local step", j, e)
+    np.testing.assert_array_equal(ctx.cb_get_central(), Z2)
+    np.testing.assert_array_equal(ctx.cb_get_prev_central(), Zp2)
 
 
 def test_sma_microbench_size_sampled():
     """The full SMA-only workload (ResNet-50's P, k = 32): the oracle
-    computes 4096 sampled parameters (plus the first and last) one by one."""
+    computes 4096 sampled parameters (plus the first and last) one by one,
+    for every replica and z."""
     k = wl.SMA_MICRO_K
     m = cb.model("resnet50", *MODEL_SHAPES["resnet50"])
     P = cb.cb_num_params(m)
@@ -168,10 +225,13 @@ def test_sma_microbench_size_sampled():
                           np.random.default_rng(1).choice(P, 4096, replace=False)])
     Wn, _, Zn, Zpn = oracle.sma_update(W[:, idx], G[:, idx], Z[idx], Zp[idx], f32(1.0 / k),
                                        f32(0.01), f32(0.9))
-    assert max_rel(ctx.cb_get_central()[idx], Zn) <= 1e-6
+    one = [(0, "all", (len(idx),))]
+    assert displacement_errors(Z[idx], ctx.cb_get_central()[idx], Z[idx], Zn, one).max() <= \
+        TOL_STEP1
     np.testing.assert_array_equal(ctx.cb_get_prev_central()[idx], Z[idx])
-    for j in (0, 13, k - 1):
-        assert max_rel(ctx.cb_get_replica(j)[idx], Wn[j]) <= 1e-6
+    for j in range(k):
+        e = displacement_errors(W[j, idx], ctx.cb_get_replica(j)[idx], W[j, idx], Wn[j], one)
+        assert e.max() <= TOL_STEP1, (j, e)
 
 
 def test_sma_kernel_invariants():
@@ -190,7 +250,7 @@ def test_sma_kernel_invariants():
     ctx.cb_sma_apply(_dev(np.zeros((k, P), np.float32)))
     np.testing.assert_array_equal(ctx.cb_get_central(), Z)
     np.testing.assert_array_equal(ctx.cb_get_prev_central(), Z)
-    for j in (0, k - 1):
+    for j in range(k):
         np.testing.assert_array_equal(ctx.cb_get_replica(j), Z)
     # conservation of the corrections, at fp32 resolution
     ctx.cb_set_state(W, Z, Zp)
@@ -204,82 +264,133 @@ def test_sma_kernel_invariants():
 
 def test_one_learner_no_correction_is_momentum_sgd():
     """k = 1, alpha = 0 with learner momentum mu is heavy-ball SGD (Eq. 3):
-    the replica follows the oracle, and z never moves from w0 (bitwise)."""
+    the replica follows the oracle step by step, and z never moves from w0
+    (bitwise)."""
     p = Pair("lenet5", 1, 28, 28, 10, k=1, b=8, alpha=0.0, mu_l=0.9, seed=5)
     for t in range(4):
         p.step(t)
+        p.check_grads(verbose=False)
         p.sync()
     np.testing.assert_array_equal(p.gpu.cb_get_central(), p.w0)
-    p.check_state(tol=TOL_AMBIGUOUS)
-    assert rel_l2(p.gpu.cb_get_replica(0), p.ref.replica(0)) <= TOL_Z_L2
+    p.summary(f"z bitwise w0, replica rel-L2 "
+              f"{np.linalg.norm(p.gpu.cb_get_replica(0) - p.ref.replica(0)) / np.linalg.norm(p.ref.replica(0)):.2e}")
+
+
+def test_no_correction_decouples_learners():
+    """alpha = 0: every replica follows an independent one-learner run on its
+    own batches (Sec. 3.2 with no correction; replica batching must not mix
+    learners).  Three learners on the GPU against three oracle runs of one
+    learner each."""
+    k, b = 3, 6
+    m = cb.model("resnet32", 3, 16, 16, 10)
+    layout = cb.cb_tensor_layout(m)
+    w0 = wl.init_w0(layout, 13)
+    ctx = cb.Context(m, k, b, 0.0, 0.01, 0.9, w0)
+    om = oracle.model("resnet32", 3, 16, 16, 10)
+    solo = [oracle.SMA(om, w0, 1, b, 0.0, f32(0.01), f32(0.9)) for _ in range(k)]
+    worst = 0.0
+    for t in range(3):
+        x, y = wl.batch(k * b, 3, 16, 16, 10, 13, t)
+        W0 = [ctx.cb_get_replica(j) for j in range(k)]
+        ctx.cb_step(_dev(x), _dev(y))
+        for j, s in enumerate(solo):
+            s.step(x[j * b:(j + 1) * b], y[j * b:(j + 1) * b])
+            res = resolve_decisions(oracle, om, s.replica(0), x[j * b:(j + 1) * b],
+                                    y[j * b:(j + 1) * b], ctx.cb_get_grad(j), layout,
+                                    g0=s.grad(0))
+            assert res["ok"], (t, j, res["err"])
+            worst = max(worst, res["err"])
+            r0 = s.replica(0)
+            if res["flips"]:
+                s.sma_apply(res["resolved"][None])
+            else:
+                s.sync()
+            solo[j] = s
+            W0[j] = (W0[j], r0, s.replica(0))
+        ctx.cb_sync()
+        for j in range(k):
+            a0, r0, r1 = W0[j]
+            e = displacement_errors(a0, ctx.cb_get_replica(j), r0, r1, layout).max()
+            assert e <= TOL_STEP1, (t, j, e)
+        np.testing.assert_array_equal(ctx.cb_get_central(), w0)
+    _report(f"alpha=0 decoupling, resnet32 16x16 k=3 b=6: worst gradient {worst:.2e}")
 
 
 # ------------------------------------------------------------- end to end
 
 def test_lenet_k2_b4_ten_iterations():
+    """The LeNet workload of 2 learners of 4 images for its 10 SMA
+    iterations: every step's gradients and every synchronisation's update
+    at 1e-4 per tensor, z at the end within 1e-3."""
     p = Pair("lenet5", 1, 28, 28, 10, k=2, b=4, seed=0)
     for t in range(10):
         p.step(t)
-        if t == 0:
-            p.check_grads()
-        p.sync()
-        if t == 0:
-            p.check_state()
-    assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
-    p.check_state(tol=1e-3)
+        p.check_grads(verbose=t == 0)
+        p.sync(verbose=t == 0)
+    err = p.z_error()
+    p.summary(f"z rel-L2 after 10 {err:.2e}")
+    assert err <= TOL_Z_L2
 
 
 def test_lenet_k8_b16_hundred_iterations():
-    """Step 1 per tensor, z at step 10 within 1e-3.  At step 100 this
-    workload is chaotic at fp32 resolution: the oracle itself drifts by the
-    stored envelope when w0 moves by one part in 1e7, so the bound there is
-    the larger of 1e-3 and twice that drift."""
-    env = json.load(open(os.path.join(GOLDEN, "lenet5_k8_b16_envelope.json")))["rel_l2"]
+    """LeNet, 8 learners of 16, 100 SMA iterations with every step's
+    gradients and updates at 1e-4 per tensor; z within 1e-3 after 10 and
+    after 100 iterations."""
     p = Pair("lenet5", 1, 28, 28, 10, k=8, b=16, seed=1)
+    errs = {}
     for t in range(100):
         p.step(t)
-        if t == 0:
-            p.check_grads(require_margin=False)
-        p.sync()
-        if t == 0:
-            p.check_state()
-        if t + 1 == 10:
-            assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
-    err = rel_l2(p.gpu.cb_get_central(), p.ref.central())
-    assert err <= max(TOL_Z_L2, 2 * env["100"]), (err, env["100"])
+        p.check_grads(verbose=t == 0)
+        p.sync(verbose=t == 0)
+        if t + 1 in (10, 100):
+            errs[t + 1] = p.z_error()
+    p.summary(f"z rel-L2 after 10 {errs[10]:.2e}, after 100 {errs[100]:.2e}")
+    assert max(errs.values()) <= TOL_Z_L2, errs
 
 
+@pytest.mark.timeout(600)
 def test_lenet_k8_b16_thousand_iterations():
     """The LeNet workload as specified: k = 8 learners of 16, 1000 SMA
-    iterations with a synchronisation every iteration, against the oracle's
-    stored central model (tests/golden/make_golden.py lenet_z1000).  The
-    oracle drifts from itself by the stored amount when w0 moves by one part
-    in 1e7, so the bound is the larger of 1e-3 and twice that drift."""
+    iterations with a synchronisation every iteration.
+
+    (1) Step by step against the oracle with ambiguous decisions resolved:
+    z within 1e-3 after 1000 iterations (and every gradient and update at
+    1e-4 per tensor on the way).  (2) Against the oracle's own stored
+    trajectory (tests/golden/make_golden.py lenet_z1000), which takes its
+    own outcome at every ambiguous decision: there the two trajectories
+    separate at fp32 resolution, as the oracle does from itself when w0
+    moves by one part in 1e7 (stored drift), so the bound is the larger of
+    1e-3 and twice that drift."""
+    wk = wl.LENET_K8
+    p = Pair(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes, k=wk.k, b=wk.b, seed=wk.seed,
+             lr=wk.lr, mu=wk.momentum)
+    for t in range(1000):
+        p.step(t)
+        p.check_grads(verbose=False)
+        p.sync(check=t % 50 == 0)
+    err = p.z_error()
     meta = json.load(open(os.path.join(GOLDEN, "lenet5_k8_b16_z1000.json")))
     z1000 = np.load(os.path.join(GOLDEN, meta["file"]))
-    wk = wl.LENET_K8
-    m = cb.model("lenet5", wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
-    ctx = cb.Context(m, wk.k, wk.b, wk.alpha, wk.lr, wk.momentum,
-                     wl.init_w0(cb.cb_tensor_layout(m), wk.seed))
-    for t in range(1000):
-        x, y = wl.workload_batch(wk, t)
-        ctx.cb_step(_dev(x), _dev(y))
-        ctx.cb_sync()
-    err = rel_l2(ctx.cb_get_central(), z1000)
-    assert err <= max(TOL_Z_L2, 2 * meta["rel_l2"]["1000"]), (err, meta["rel_l2"])
+    err_gold = float(np.linalg.norm(p.gpu.cb_get_central() - z1000) / np.linalg.norm(z1000))
+    bound = max(TOL_Z_L2, 2 * meta["rel_l2"]["1000"])
+    p.summary(f"z rel-L2 after 1000: resolved {err:.2e}; against the stored trajectory "
+              f"{err_gold:.2e} (bound {bound:.2e}, the oracle's own drift "
+              f"{meta['rel_l2']['1000']:.2e})")
+    assert err <= TOL_Z_L2
+    assert err_gold <= bound
 
 
 def test_lenet_learner_momentum_and_unsynced_steps():
     p = Pair("lenet5", 1, 28, 28, 10, k=3, b=5, mu_l=0.9, seed=5)
     p.step(0)
     p.check_grads()
-    p.sync()
-    p.check_state()
+    p.sync(verbose=True)
     p.step(1)
+    p.check_grads()
     p.step(2)  # no sync in between: a local step first
-    p.check_grads(require_margin=False)
-    p.sync()
-    p.check_state(tol=TOL_AMBIGUOUS)
+    p.check_grads()
+    p.sync(verbose=True)
+    p.summary()
 
 
 def test_control_between_iterations():
@@ -287,14 +398,15 @@ def test_control_between_iterations():
     (Sec. 3.2) between iterations, on the GPU and in the oracle: a LeNet job
     with capacity 4 goes 2 -> 3 -> 1 -> 4 learners.  New replicas start
     bitwise at z, a restart puts every replica and z_prev bitwise at z, and
-    the state tracks the oracle after every phase."""
-    p = Pair("lenet5", 1, 28, 28, 10, k=4, b=5, seed=5)
+    every gradient and update matches the oracle at 1e-4 per tensor."""
+    p = Pair("lenet5", 1, 28, 28, 10, k=4, b=5, seed=5, tag="lenet5 control")
     t = 0
 
     def run(n):
         nonlocal t
         for _ in range(n):
             p.step(t)
+            p.check_grads(verbose=False)
             p.sync()
             t += 1
 
@@ -305,16 +417,13 @@ def test_control_between_iterations():
 
     resize(2)
     run(2)
-    p.check_state(tol=TOL_AMBIGUOUS)
     z = p.gpu.cb_get_central()
     resize(3)
     np.testing.assert_array_equal(p.gpu.cb_get_replica(2), z)
     run(2)
-    p.check_state(tol=TOL_AMBIGUOUS)
     p.gpu.cb_set_lr(0.03)
     p.ref.set_lr(f32(0.03))
     run(1)
-    p.check_state(tol=TOL_AMBIGUOUS)
     p.gpu.cb_restart()
     p.ref.restart()
     z = p.gpu.cb_get_central()
@@ -326,8 +435,9 @@ def test_control_between_iterations():
     run(1)
     resize(4)
     run(1)
-    p.check_state(tol=TOL_AMBIGUOUS)
-    assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
+    err = p.z_error()
+    p.summary(f"z rel-L2 {err:.2e}")
+    assert err <= TOL_Z_L2
     # resizing needs an iteration barrier, and the capacity bounds k
     p.step(t)
     with pytest.raises(cb.CBError):
@@ -340,73 +450,69 @@ def test_control_between_iterations():
 def test_ea_sgd_mode_and_sync_interval():
     """mu = 0 (synchronous elastic averaging, the comparison of Sec. 5.5)
     with a sync interval of 3: two local steps, then a synchronisation."""
-    p = Pair("lenet5", 1, 28, 28, 10, k=3, b=5, mu=0.0, seed=5)
+    p = Pair("lenet5", 1, 28, 28, 10, k=3, b=5, mu=0.0, seed=5, tag="lenet5 EA-SGD tau=3")
     for t in range(6):
         p.step(t)
+        p.check_grads(verbose=False)
         if t % 3 == 2:
-            p.sync()
-    p.check_state(tol=TOL_AMBIGUOUS)
-    assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
+            p.sync(verbose=True)
+    err = p.z_error()
+    p.summary(f"z rel-L2 {err:.2e}")
+    assert err <= TOL_Z_L2
 
 
 def test_resnet32_ragged_batch():
     """Every ResNet-32 path (stride-2 option-A blocks, BN, average pool) with
-    3 images per learner: partial tiles in every GEMM; 16x16 images and a
-    seed whose decisions are all unambiguous."""
+    3 images per learner: partial tiles in every GEMM; 16x16 images."""
     p = Pair("resnet32", 3, 16, 16, 10, k=2, b=3, seed=1)
-    p.step(0)
-    p.check_grads()
-    p.sync()
-    p.check_state()
-    for t in range(1, 3):
+    for t in range(3):
         p.step(t)
-        p.check_grads_at_gpu_replicas()
-        p.sync()
-    assert rel_l2(p.gpu.cb_get_central(), p.ref.central()) <= TOL_Z_L2
+        p.check_grads()
+        p.sync(verbose=True)
+    p.summary(f"z rel-L2 {p.z_error():.2e}")
 
 
 def test_resnet32_odd_feature_maps():
     """28 x 28 images: stage 3 runs on 7 x 7 maps (the implicit-GEMM paths
     with odd sizes, a global average over 49 pixels)."""
     p = Pair("resnet32", 3, 28, 28, 10, k=2, b=3, seed=2)
-    p.step(0)
-    p.check_grads_at_gpu_replicas()
-    p.sync()
-    p.check_state(tol=TOL_AMBIGUOUS)
+    for t in range(2):
+        p.step(t)
+        p.check_grads()
+        p.sync(verbose=True)
+    p.summary()
 
 
-def test_resnet32_k4_b32_full_size_learners():
-    """Full-size ResNet-32 workload; the oracle recomputes learners 0 and 3.
-    At 32 images x 32x32 some ReLU decision is always within fp32 rounding
-    of zero, so the gradients take the ambiguity bound; the losses are
-    strict."""
-    k, b = 4, 32
-    m = cb.model("resnet32", 3, 32, 32, 10)
-    layout = cb.cb_tensor_layout(m)
-    w0 = wl.init_w0(layout, wl.RESNET32_K4.seed)
-    ctx = cb.Context(m, k, b, 0.25, 0.01, 0.9, w0)
-    x, y = wl.workload_batch(wl.RESNET32_K4, 0)
-    ctx.cb_step(_dev(x), _dev(y))
-    loss = ctx.cb_get_loss()
-    om = oracle.model("resnet32", 3, 32, 32, 10)
-    for j in (0, 3):
-        xj, yj = x[j * b:(j + 1) * b], y[j * b:(j + 1) * b]
-        lj, gj = oracle.learner_grad(om, w0, xj, yj)
-        assert abs(loss[j] - lj) / abs(lj) <= TOL_STEP1
-        margin = oracle.learner_margin(om, w0, xj, yj)
-        tol = TOL_STEP1 if margin >= MARGIN else TOL_AMBIGUOUS
-        err, where = per_tensor_max_rel(ctx.cb_get_grad(j), gj, layout)
-        assert err <= tol, (j, err, where, "margin", margin)
+@pytest.mark.timeout(900)
+def test_resnet32_k4_b32_full_size():
+    """The ResNet-32 workload at full size (k = 4 learners of 32 images,
+    32 x 32): two SMA iterations with every learner's loss and gradient and
+    every update of the replicas and z compared at 1e-4 per tensor.  After
+    the first synchronisation z is w0 bitwise (all corrections are 0); the
+    second moves it by the mean of the first step's updates."""
+    wk = wl.RESNET32_K4
+    p = Pair(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes, k=wk.k, b=wk.b, seed=wk.seed,
+             lr=wk.lr, mu=wk.momentum, tag="resnet32 k=4 b=32")
+    for t in range(2):
+        p.step(t)
+        p.check_grads()
+        p.sync(verbose=True)
+        if t == 0:
+            np.testing.assert_array_equal(p.gpu.cb_get_central(), p.w0)
+    p.summary(f"z rel-L2 after 2 {p.z_error():.2e}")
 
 
 def test_resnet32_k4_b32_hundred_iterations():
     """The full ResNet-32 workload (k = 4 learners of 32 images) for 100 SMA
-    iterations against the oracle's central model stored after 10 and after
-    100 of the same iterations (tests/golden/make_golden.py resnet32_z10,
-    resnet32_z100).  At step 10, relative L2 <= 1e-3.  At step 100 the
-    oracle itself drifts by more than that when w0 moves by one part in 1e7
-    (resnet32_envelope), so the bound there is the larger of 1e-3 and twice
-    that drift."""
+    iterations against the oracle's own central model stored after 10 and
+    after 100 of the same iterations (tests/golden/make_golden.py
+    resnet32_z10, resnet32_z100).  At step 10, relative L2 <= 1e-3.  The
+    stored trajectory takes the oracle's own outcome at every ambiguous
+    decision, so the two separate at fp32 resolution; by step 100 the oracle
+    itself drifts by more than 1e-3 when w0 moves by one part in 1e7
+    (resnet32_envelope), and the bound there is the larger of 1e-3 and
+    twice that drift.  (The decision-resolved comparison at full size is
+    test_resnet32_k4_b32_full_size.)"""
     wk = wl.RESNET32_K4
     env = json.load(open(os.path.join(GOLDEN, "resnet32_k4_b32_envelope.json")))["rel_l2"]
     z = {}
@@ -416,23 +522,30 @@ def test_resnet32_k4_b32_hundred_iterations():
     m = cb.model("resnet32", wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
     layout = cb.cb_tensor_layout(m)
     ctx = cb.Context(m, wk.k, wk.b, wk.alpha, wk.lr, wk.momentum, wl.init_w0(layout, wk.seed))
+    errs = {}
     for t in range(100):
         x, y = wl.workload_batch(wk, t)
         ctx.cb_step(_dev(x), _dev(y))
         ctx.cb_sync()
-        if t + 1 == 10:
-            err10 = rel_l2(ctx.cb_get_central(), z[10])
-            assert err10 <= TOL_Z_L2, err10
-    err = rel_l2(ctx.cb_get_central(), z[100])
-    assert err <= max(TOL_Z_L2, 2 * env["100"]), (err, env["100"])
+        if t + 1 in z:
+            errs[t + 1] = float(np.linalg.norm(ctx.cb_get_central() - z[t + 1]) /
+                                np.linalg.norm(z[t + 1]))
+    bound = max(TOL_Z_L2, 2 * env["100"])
+    _report(f"resnet32 k=4 b=32, 100 iterations against the stored trajectory: z rel-L2 after "
+            f"10 {errs[10]:.2e} (bound {TOL_Z_L2:.0e}), after 100 {errs[100]:.2e} (bound "
+            f"{bound:.2e}; the oracle's own drift {env['10']:.2e} / {env['100']:.2e})")
+    assert errs[10] <= TOL_Z_L2
+    assert errs[100] <= bound
 
 
+@pytest.mark.timeout(900)
 def test_resnet32_k32_b16_full_size_learners():
     """The largest point of the k sweep: 32 ResNet-32 learners of 16 images
     in every launch (other tile choices and grids than at k = 4).  The
-    oracle recomputes learners 0, 17 and 31; losses strict, gradients with
-    the margin rule; then one synchronisation against the SMA kernel's
-    oracle on the GPU's own gradients."""
+    oracle recomputes learners 0, 17 and 31: loss and gradient at 1e-4 per
+    tensor with ambiguous decisions resolved, and the synchronisation's
+    update of those replicas (-lr times the gradient, all corrections being
+    0 at the first step) at 1e-4 per tensor; z stays w0 bitwise."""
     k, b = 32, 16
     wk = wl.RESNET32_SWEEP.with_k(k)
     m = cb.model("resnet32", 3, 32, 32, 10)
@@ -443,33 +556,41 @@ def test_resnet32_k32_b16_full_size_learners():
     ctx.cb_step(_dev(x), _dev(y))
     loss = ctx.cb_get_loss()
     om = oracle.model("resnet32", 3, 32, 32, 10)
+    resolved = {}
     for j in (0, 17, 31):
         xj, yj = x[j * b:(j + 1) * b], y[j * b:(j + 1) * b]
         lj, gj = oracle.learner_grad(om, w0, xj, yj)
-        assert abs(loss[j] - lj) / abs(lj) <= TOL_STEP1
-        margin = oracle.learner_margin(om, w0, xj, yj)
-        tol = TOL_STEP1 if margin >= MARGIN else TOL_AMBIGUOUS
-        err, where = per_tensor_max_rel(ctx.cb_get_grad(j), gj, layout)
-        assert err <= tol, (j, err, where, "margin", margin)
-    G = np.stack([ctx.cb_get_grad(j) for j in range(k)])
+        lerr = abs(loss[j] - lj) / abs(lj)
+        assert lerr <= TOL_STEP1
+        res = resolve_decisions(oracle, om, w0, xj, yj, ctx.cb_get_grad(j), layout, g0=gj)
+        _report(describe(f"resnet32 k=32 b=16 learner {j}", res, lerr))
+        assert res["ok"], (j, res["err"])
+        resolved[j] = res["resolved"]
     ctx.cb_sync()
-    W = np.tile(w0, (k, 1))
-    Wn, _, Zn, _ = oracle.sma_update(W, G, w0, w0, f32(1.0 / k), f32(wk.lr), f32(wk.momentum))
-    assert max_rel(ctx.cb_get_central(), Zn) <= 1e-6
-    for j in (0, 31):
-        assert max_rel(ctx.cb_get_replica(j), Wn[j]) <= 1e-6
+    np.testing.assert_array_equal(ctx.cb_get_central(), w0)
+    lr = f32(wk.lr)
+    for j, g in resolved.items():
+        e = displacement_errors(w0, ctx.cb_get_replica(j), w0, w0 - lr * g, layout).max()
+        _report(f"resnet32 k=32 b=16 learner {j}: update of the replica {e:.2e}")
+        assert e <= TOL_STEP1, (j, e)
 
 
 def test_resnet50_k2_b32_full_size_learner0():
     """Full-size ResNet-50 workload (k = 2 learners of 32 images, 224x224):
     learner 0's loss and sampled gradient entries against the oracle's
-    stored values (tests/golden/make_golden.py resnet50_sampled).  The loss
-    is strict.  The last stage normalises 49 pixels per image and channel,
-    so a single ReLU decision within fp32 rounding of zero moves a channel's
-    gradient sum by a visible share; the gradients take the ambiguity
-    bound (every ResNet-50 operator is strict at these shapes in
-    test_gpu_kernels.py)."""
+    stored values (tests/golden/make_golden.py resnet50_sampled).
+
+    The loss is held to 1e-4.  A learner here takes about 800 ReLU and
+    max-pool decisions within rounding of turning, too many to resolve one
+    by one at ~10 minutes of oracle time per gradient, so the sampled
+    gradients are held to what the oracle itself does under rounding-sized
+    noise: per tensor, the larger of 1e-4 and twice the largest error of the
+    oracle's own sampled gradient at w0*(1+1e-7 N(0,1)) over three draws
+    (make_golden.py resnet50_envelope).  Every ResNet-50 operator is held to
+    1e-4 at these shapes in test_gpu_kernels.py."""
     gold = json.load(open(os.path.join(GOLDEN, "resnet50_k2_b32_learner0.json")))
+    envs = [json.load(open(os.path.join(GOLDEN, f"resnet50_k2_b32_envelope{i}.json")))
+            for i in range(3)]
     wk = wl.RESNET50_K2
     m = cb.model(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
     w0 = wl.init_w0(cb.cb_tensor_layout(m), wk.seed)
@@ -477,16 +598,25 @@ def test_resnet50_k2_b32_full_size_learner0():
     x, y = wl.workload_batch(wk, 0)
     ctx.cb_step(_dev(x), _dev(y))
     loss = ctx.cb_get_loss()
-    assert abs(loss[0] - gold["loss"]) / gold["loss"] <= TOL_STEP1
+    lerr = abs(loss[0] - gold["loss"]) / gold["loss"]
+    assert lerr <= TOL_STEP1
     g = ctx.cb_get_grad(0)
-    worst = 0.0
-    for t in gold["tensors"]:
+    worst, worst_rl, above, n_env = 0.0, 0.0, 0, 0
+    for i, t in enumerate(gold["tensors"]):
         idx = np.array(t["index"])
-        err = np.abs(g[idx] - np.array(t["value"])).max() / t["max_abs"]
-        worst = max(worst, err)
-        assert err <= TOL_AMBIGUOUS, (t["offset"], t["kind"], t["shape"], err)
-    print(f"resnet50 k2 b32: loss rel err {abs(loss[0] - gold['loss']) / gold['loss']:.2e}, "
-          f"worst sampled gradient {worst:.2e}")
+        ref = np.array(t["value"])
+        d = g[idx] - ref
+        err = np.abs(d).max() / t["max_abs"]
+        rl = np.linalg.norm(d) / max(np.linalg.norm(ref), 1e-300)
+        env = max(e["tensors"][i]["max_rel"] for e in envs)
+        bound = max(TOL_STEP1, 2 * env)
+        n_env += env > TOL_STEP1
+        above += err > TOL_STEP1
+        worst, worst_rl = max(worst, err), max(worst_rl, rl)
+        assert err <= bound, (t["offset"], t["kind"], t["shape"], err, env)
+    _report(f"resnet50 k=2 b=32 learner 0: loss {lerr:.2e} | sampled gradients: worst max-rel "
+            f"{worst:.2e}, worst rel-L2 {worst_rl:.2e}; {above} of {len(gold['tensors'])} tensors "
+            f"above 1e-4 (the oracle's own drift exceeds 1e-4 in {n_env})")
 
 
 def test_replicas_are_independent_and_batched():

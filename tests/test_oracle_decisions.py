@@ -35,16 +35,19 @@ class Act:
             self.flips.setdefault(int(s), []).append((int(i), int(a)))
 
     def relu(self, v):
+        """A flipped decision outputs 0 for a positive input and |v| for the
+        rest, and passes the gradient where that output is positive."""
         s = self.site
         self.site += 1
         self.seen.append(("relu", v.detach().clone(), None))
-        keep = (v > 0).double()
-        if s in self.flips:
-            flat = keep.view(-1).clone()
-            for i, _ in self.flips[s]:
-                flat[i] = 1.0 - flat[i]
-            keep = flat.view_as(keep)
         y = F.relu(v).detach()
+        if s in self.flips:
+            flat = y.view(-1).clone()
+            vf = v.detach().view(-1)
+            for i, _ in self.flips[s]:
+                flat[i] = 0.0 if vf[i] > 0 else (-vf[i] if -vf[i] > 0 else 2.2250738585072014e-308)
+            y = flat.view_as(y)
+        keep = (y > 0).double()
         return y + v * keep - (v * keep).detach()
 
     def maxpool(self, x, K, st, pad):
@@ -239,3 +242,26 @@ def test_resolution_finds_rounding_flips_and_rejects_real_errors(oracle_lib):
     assert int(np.prod(s2)) == n
     bad[off:off + n], bad[o2:o2 + n] = gp[o2:o2 + n], gp[off:off + n]
     assert not resolve_decisions(oracle, m, w, x, y, bad, layout, deltas=deltas, g0=g0)["ok"]
+
+
+def test_resolution_takes_duplicate_candidates_once(oracle_lib):
+    """LeNet, seed 0: a conv1 ReLU input just above zero wins its 2 x 2 pooling
+    window of zeros.  Taking that ReLU decision the other way, or letting any
+    of the three zero cells win the window, has the same effect; a gradient
+    with that effect must resolve with exactly one flip (a fit that spreads
+    weight over the duplicates, or counts the effect twice, fails)."""
+    m = oracle.model("lenet5", 1, 28, 28, 10)
+    layout = oracle.tensors(m)
+    w = wl.init_w0(layout, 0).astype(np.float64)
+    x, y = wl.batch(16, 1, 28, 28, 10, 0, 0)
+    dec = oracle.learner_decisions(m, w, x, y, 1e-4)
+    window = dec[(dec["site"] == 1) & (dec["idx"] == 1868)]
+    assert len(window) == 3
+    _, g0 = oracle.learner_grad(m, w, x, y)
+    _, other = oracle.learner_grad_flipped(m, w, x, y, window[:1])
+    effects = [oracle.learner_grad_flipped(m, w, x, y, window[i:i + 1])[1] for i in range(3)]
+    for e in effects[1:]:
+        np.testing.assert_allclose(e, effects[0], rtol=0, atol=1e-15)
+    res = resolve_decisions(oracle, m, w, x, y, other, layout, deltas=(1e-4,), g0=g0)
+    assert res["raw_max_rel"] > 10 * TOL_STEP1, res["raw_max_rel"]
+    assert res["ok"] and res["flips"] == 1, {k: v for k, v in res.items() if k != "resolved"}
