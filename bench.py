@@ -22,6 +22,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+SWEEP_BEYOND = (48, 64, 96, 128)  # learner counts past the workload's sweep
 FP32_MFMA_PEAK_TFS = 157.3   # MI355X dense fp32 matrix
 
 
@@ -89,8 +90,10 @@ def roofline_of(prof):
             "frac": round(ach / HBM_PEAK_GBS, 4), **base}
 
 
-def time_training(wk, steps, warmup, ring=8, prof_steps=0):
-    """ms per SMA iteration (cb_step + cb_sync) for workload wk."""
+def time_training(wk, steps, warmup, ring=8, prof_steps=0, repeats=1):
+    """ms per SMA iteration (cb_step + cb_sync) for workload wk: the median
+    over `repeats` timed runs of `steps` iterations (all runs kept in
+    time_training.last_repeats)."""
     import torch
     import paper_1901_02244_amd as cb
     import workloads as wl
@@ -104,16 +107,21 @@ def time_training(wk, steps, warmup, ring=8, prof_steps=0):
         ctx.cb_step(xs[i % n], ys[i % n])
         ctx.cb_sync()
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    ev0.record()
-    for i in range(steps):
-        ctx.cb_step(xs[i % n], ys[i % n])
-        ctx.cb_sync()
-    ev1.record()
-    torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) * 1e3 / steps
-    ms = ev0.elapsed_time(ev1) / steps
+    runs, walls = [], []
+    for _ in range(repeats):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        ev0.record()
+        for i in range(steps):
+            ctx.cb_step(xs[i % n], ys[i % n])
+            ctx.cb_sync()
+        ev1.record()
+        torch.cuda.synchronize()
+        walls.append((time.perf_counter() - t0) * 1e3 / steps)
+        runs.append(ev0.elapsed_time(ev1) / steps)
+    order = sorted(range(repeats), key=lambda i: runs[i])
+    ms, wall = runs[order[repeats // 2]], walls[order[repeats // 2]]
+    time_training.last_repeats = runs
     loss = ctx.cb_get_loss()
     prof = None
     if prof_steps:
@@ -337,10 +345,7 @@ def cpu_baseline(wk, iters=3):
     import workloads as wl
 
     n_host = os.cpu_count()
-    try:
-        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
-    except (AttributeError, OSError):
-        pass
+    _pin_one_core()
     m = oracle.model(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
     w0 = wl.init_w0(oracle.tensors(m), wk.seed)
     ref = oracle.SMA(m, w0, wk.k, wk.b, wk.alpha, wk.lr, wk.momentum)
@@ -357,6 +362,90 @@ def cpu_baseline(wk, iters=3):
                       f"host cores ({cpu_model()})"}
 
 
+def _pin_one_core():
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+    except (AttributeError, OSError):
+        pass
+
+
+def cpu_baselines_by_config():
+    """The oracle (single-threaded C, one host core) on a bounded sample of
+    every workload, same inputs as the GPU runs: images/s, or GB/s of the
+    synchronisation for the SMA-only microbenchmark.  Each sample is a few
+    to ~25 s of CPU work; what it covers is stated with it."""
+    import dataclasses
+
+    import numpy as np
+    import oracle
+    import workloads as wl
+
+    _pin_one_core()
+    n_host = os.cpu_count()
+    where = f"single-threaded on 1 of {n_host} host cores ({cpu_model()})"
+    out = {}
+
+    def sma_run(wk, iters, k=None, learners=None):
+        """iters SMA iterations of wk (k learners); with learners, only the
+        first `learners` learners' gradients are timed (the sample), plus the
+        synchronisation of all k replicas."""
+        m = oracle.model(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
+        w0 = wl.init_w0(oracle.tensors(m), wk.seed)
+        k = k or wk.k
+        if learners is None:
+            ref = oracle.SMA(m, w0, k, wk.b, 1.0 / k, wk.lr, wk.momentum)
+            t0 = time.perf_counter()
+            for t in range(iters):
+                x, y = wl.batch(k * wk.b, wk.in_c, wk.in_h, wk.in_w, wk.num_classes, wk.seed, t)
+                ref.step(x, y)
+                ref.sync()
+            return time.perf_counter() - t0, iters * k * wk.b
+        x, y = wl.batch(k * wk.b, wk.in_c, wk.in_h, wk.in_w, wk.num_classes, wk.seed, 0)
+        P = oracle.num_params(m)
+        W = np.tile(w0.astype(np.float64), (k, 1))
+        t0 = time.perf_counter()
+        G = np.zeros((k, P))
+        for j in range(learners):
+            _, G[j] = oracle.learner_grad(m, W[j], x[j * wk.b:(j + 1) * wk.b],
+                                          y[j * wk.b:(j + 1) * wk.b])
+        oracle.sma_update(W, G, w0, w0, 1.0 / k, wk.lr, wk.momentum)
+        return time.perf_counter() - t0, learners * wk.b
+
+    for name, wk, iters in (("lenet5_k2_b4", wl.LENET_K2, 10), ("lenet5_k8_b16", wl.LENET_K8, 100)):
+        dt, imgs = sma_run(wk, iters)
+        out[name] = {"value": round(imgs / dt, 2), "unit": "images/s", "cores": 1, "kind": "oracle",
+                     "sample": f"{iters} SMA iterations ({imgs} images, all {wk.k} learners + "
+                               f"sync) in {dt:.1f} s, {where}"}
+        log(f"[bench] cpu {name}: {out[name]['value']} images/s")
+    sw = wl.RESNET32_SWEEP
+    dt, imgs = sma_run(sw, 1, k=32, learners=2)
+    out["resnet32_b16_k32"] = {
+        "value": round(imgs / dt, 2), "unit": "images/s", "cores": 1, "kind": "oracle",
+        "sample": f"one SMA iteration of 32 learners of 16: the gradients of 2 learners "
+                  f"({imgs} images) and the synchronisation of all 32 replicas, in {dt:.1f} s, "
+                  f"{where}; the other learners' gradients cost the same per image"}
+    log(f"[bench] cpu resnet32 k=32 b=16: {out['resnet32_b16_k32']['value']} images/s")
+    r50 = dataclasses.replace(wl.RESNET50_K2, b=2)
+    dt, imgs = sma_run(r50, 1, k=2, learners=1)
+    out["resnet50_k2_b32"] = {
+        "value": round(imgs / dt, 3), "unit": "images/s", "cores": 1, "kind": "oracle",
+        "sample": f"the gradient of one learner of 2 images at 224 x 224 (of the workload's 2 x 32) "
+                  f"and a synchronisation of 2 replicas, in {dt:.1f} s, {where}"}
+    log(f"[bench] cpu resnet50: {out['resnet50_k2_b32']['value']} images/s")
+    k, cols = wl.SMA_MICRO_K, 1 << 20
+    W, G, Z, Zp = wl.random_state(k, cols, seed=7)
+    t0 = time.perf_counter()
+    oracle.sma_update(W, G, Z, Zp, 1.0 / k, 0.01, 0.9)
+    dt = time.perf_counter() - t0
+    nbytes = 4 * cols * (3 * k + 4)
+    out["sma_micro"] = {
+        "value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+        "sample": f"one synchronisation of {k} replicas on {cols} of the {wl.SMA_MICRO_P} "
+                  f"parameters ({nbytes} algorithmic fp32 bytes, 4P(3k+4)) in {dt:.2f} s, {where}"}
+    log(f"[bench] cpu sma micro: {out['sma_micro']['value']} GB/s")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -367,6 +456,10 @@ def main():
     ap.add_argument("--no-micro", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--prof-steps", type=int, default=100)
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="timed runs of the headline workload; the median is reported")
+    ap.add_argument("--only", choices=("lenet", "resnet50", "sma"),
+                    help="run only this workload (for profiling) and print its figures")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run one plain copy kernel of this many MiB (read and written once "
                          "each), the reference dispatch for HBM byte counters")
@@ -390,9 +483,15 @@ def main():
         log(f"[bench] copy kernel: {n * 4} bytes read, {n * 4} bytes written")
         del src, dst
         torch.cuda.empty_cache()
+    if args.only:
+        fn = {"lenet": lenet_latency, "resnet50": resnet50_throughput, "sma": sma_micro}[args.only]
+        print(json.dumps({"only": args.only, **fn()}), flush=True)
+        return
     wk = wl.RESNET32_K4
-    log(f"[bench] {wk.name}: warmup {args.warmup}, steps {args.steps}")
-    ms, wall, loss, prof = time_training(wk, args.steps, args.warmup, prof_steps=args.prof_steps)
+    log(f"[bench] {wk.name}: warmup {args.warmup}, steps {args.steps} x {args.repeats} repeats")
+    ms, wall, loss, prof = time_training(wk, args.steps, args.warmup, prof_steps=args.prof_steps,
+                                         repeats=args.repeats)
+    repeats_ms = [round(v, 4) for v in time_training.last_repeats]
     value = wk.n_images / (ms / 1e3)
     log(f"[bench] {wk.name}: {ms:.3f} ms/step (wall {wall:.3f}), {value:.0f} images/s")
     roof = roofline_of(prof)
@@ -422,7 +521,8 @@ def main():
     sweep = {}
     if not args.no_sweep:
         base = wl.RESNET32_SWEEP
-        for k in base.sweep_k:
+        # the workload's k values, then larger ones until throughput stops rising
+        for k in base.sweep_k + SWEEP_BEYOND:
             w = base.with_k(k)
             sms, swall, _ = time_training(w, args.sweep_steps, 3)
             sweep[str(k)] = {"ms_per_step": round(sms, 4), "images_per_s": round(w.n_images / (sms / 1e3), 1)}
@@ -438,10 +538,11 @@ def main():
     if not args.no_micro:
         micro = sma_micro()
         log(f"[bench] SMA micro: {micro}")
-    cpu = None
+    cpu, cpu_all = None, None
     if not args.no_cpu:
         cpu = cpu_baseline(wk)
         log(f"[bench] cpu baseline: {cpu}")
+        cpu_all = cpu_baselines_by_config()
 
     out = {
         "metric": "training images/sec/GPU (all k replicas) vs k; fused SMA kernel HBM GB/s",
@@ -451,6 +552,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "repeats_ms_per_step": repeats_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -459,7 +561,8 @@ def main():
         "config": {"workload": f"{wk.name}: ResNet-32 replicas, 32x32x3 N(0,1) images, 10 classes, "
                                f"k={wk.k} learners x b={wk.b}, alpha=1/k, lr={wk.lr}, mu={wk.momentum}, "
                                "one SMA iteration per step",
-                   "k": wk.k, "b": wk.b, "images_per_step": wk.n_images},
+                   "k": wk.k, "b": wk.b, "images_per_step": wk.n_images,
+                   "timing": f"median of {args.repeats} runs of {args.steps} iterations"},
         "roofline": roof,
         "step_mfma_utilisation": step_util,
         "kernels_per_step": kernels,
@@ -468,6 +571,7 @@ def main():
         **extra,
         "sma_microbench": micro,
         "cpu_baseline": cpu,
+        "cpu_baseline_by_config": cpu_all,
         "final_loss": [round(float(v), 4) for v in loss],
     }
     print(json.dumps(out), flush=True)

@@ -120,8 +120,11 @@ def resolve_decisions(oracle, om, w, x, y, g, layout, tol=TOL_STEP1, deltas=DELT
         pick = _pick_flips(D, r)
         resolved = g0 + (D @ pick) / scale
         mr, _ = tensor_errors(g, resolved, layout)
+        top = np.argsort(-mr)[:4]
         out.update(flips=int(pick.sum()), candidates=len(keys), delta=delta,
-                   err=float(mr.max()), ok=bool(mr.max() <= tol), resolved=resolved)
+                   err=float(mr.max()), ok=bool(mr.max() <= tol), resolved=resolved,
+                   worst=[(int(i), layout[i][1], tuple(layout[i][2]), float(f"{raw_mr[i]:.3g}"),
+                           float(f"{mr[i]:.3g}")) for i in top])
         if out["ok"]:
             return out
     return out
@@ -161,7 +164,7 @@ def describe(tag, res, loss_err=None, margin=None):
     return s
 
 
-def displacement_errors(a0, a1, r0, r1, layout):
+def displacement_errors(a0, a1, r0, r1, layout, carry=None):
     """Per tensor, how far an update of the GPU's state (a0 -> a1, fp32
     values) departs from the oracle's update of the same state (r0 -> r1):
     max over elements of (|da - dr| - slack) / max|dr|, with da = a1 - a0,
@@ -170,12 +173,18 @@ def displacement_errors(a0, a1, r0, r1, layout):
     update of a few parts in 1e4 of a weight cannot be resolved finer than
     its storage).  Comparing displacements rather than the state itself
     keeps an update that is small next to the weights (lr = 0.01) visible at
-    the 1e-4 bar."""
+    the 1e-4 bar.  carry (elementwise, optional) bounds how much of the
+    difference comes from the start states already differing: an update
+    of Algorithm 1 depends on the state through alpha (w - z) and the
+    momentum terms, so states apart by rounding give updates apart by those
+    coefficients times that distance."""
     a0 = np.asarray(a0, dtype=np.float32)
     a1 = np.asarray(a1, dtype=np.float32)
     da = a1.astype(np.float64) - a0.astype(np.float64)
     dr = np.asarray(r1, dtype=np.float64) - np.asarray(r0, dtype=np.float64)
     slack = 2.0 * np.spacing(np.maximum(np.abs(a0), np.abs(a1))).astype(np.float64)
+    if carry is not None:
+        slack = slack + carry
     excess = np.maximum(np.abs(da - dr) - slack, 0.0)
     out = []
     for off, n, _, _ in _tensors(layout):

