@@ -41,7 +41,7 @@ extern "C" {
 /* Version of this interface: raised with every change to a declaration
  * below.  cb_abi_version() returns the value the library was built with;
  * a caller built against another version must not call anything else. */
-#define CB_ABI_VERSION 2
+#define CB_ABI_VERSION 3
 int cb_abi_version(void);
 
 typedef struct cb_ctx cb_ctx;
@@ -326,6 +326,26 @@ int cb_test_head(int k, int b, int C, int H, int W, int classes, const float* y,
 int cb_test_softmax_xent(int k, int b, int classes, const float* logits, const int32_t* labels,
                          float* dlogits, float* loss, void* stream);
 
+/* --- for callers that cannot allocate ----------------------------------
+ * For code under HIP graph capture, tight serving loops and harnesses that
+ * forbid allocation: cb_test_conv with the scratch of its weight gradient
+ * (the split-contraction partials) taken from device memory the library
+ * holds instead of from the caller -- a static array of
+ * CB_STATIC_SCRATCH_BYTES (enough for every layer of the three workloads),
+ * one per GPU, kept until the process ends.  The caller still passes every
+ * input and output, as for cb_test_conv.  Allocates nothing (the first call
+ * on a device looks up the array's address there).  CB_ENOMEM, with a
+ * message from cb_last_error(NULL), if the layer needs more scratch than
+ * that (cb_test_conv_scratch_bytes() tells).  The array keeps the last
+ * call's contents; nothing it holds is read before the same call writes it.
+ * Calls that overlap on one GPU -- on different streams, or from different
+ * threads -- share the array and race. */
+#define CB_STATIC_SCRATCH_BYTES (32u << 20)
+int cb_test_conv_static(int k, int b, int Ci, int H, int W, int Co, int R, int stride, int pad,
+                        int relu, int has_bias, const float* x, const float* params,
+                        int64_t pstride, float* y, double* stats, const float* dy, float* dx,
+                        float* grads, void* stream);
+
 /* --- instrumentation --------------------------------------------------- */
 
 /* While enabled, every kernel launch of the context carries a start/stop
@@ -352,7 +372,8 @@ int cb_profile_entry(cb_ctx* c, int i, const char** name, int64_t* launches, dou
 int cb_profile_clear(cb_ctx* c);
 
 /* Message for the last error on this context ("" if none); valid until the
- * next call on it.  A NULL context gives the last cb_create failure. */
+ * next call on it.  A NULL context gives the last failure of a call made
+ * without one (cb_create, cb_test_conv_static). */
 const char* cb_last_error(const cb_ctx* c);
 
 /* Frees the context's host-side state; the caller then frees the workspace. */

@@ -27,11 +27,11 @@ KIND_NAMES = {0: "conv_w", 1: "bias", 2: "bn_gamma", 3: "bn_beta", 4: "fc_w"}
 
 # The interface version these bindings are written for (CB_ABI_VERSION in
 # include/crossbow_sma.h); a library built from other sources is refused.
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 # every symbol the header declares
 EXPORTS = (
-    "cb_abi_version", "cb_local_apply", "cb_test_conv_fwd_parts", "cb_test_head_ok",
+    "cb_abi_version", "cb_local_apply", "cb_test_conv_static", "cb_test_conv_fwd_parts", "cb_test_head_ok",
     "cb_test_head", "cb_num_params", "cb_num_tensors", "cb_tensor_info", "cb_workspace_bytes", "cb_create",
     "cb_step", "cb_sync", "cb_wait", "cb_get_central", "cb_get_replica", "cb_get_prev_central",
     "cb_get_grad", "cb_get_loss", "cb_sma_apply", "cb_set_state", "cb_last_error", "cb_destroy",
@@ -117,6 +117,8 @@ def lib():
         L.cb_test_conv_fwd_parts.argtypes = [_i] * 9
         L.cb_test_conv.argtypes = [_i] * 11 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P, _P, _P,
                                                ctypes.c_size_t, _P]
+        L.cb_test_conv_static.argtypes = [_i] * 11 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P,
+                                                      _P, _P]
         L.cb_test_head_ok.argtypes = [_i] * 4
         L.cb_test_head.argtypes = [_i] * 6 + [_P, _P, ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P,
                                               _P, _i, _P, _P]

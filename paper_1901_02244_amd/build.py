@@ -16,7 +16,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libcrossbow_sma.so")
-SOURCES = ["api.hip", "conv_gemm.hip", "conv_direct.hip", "layers.hip", "sma.hip", "test_hooks.hip"]
+SOURCES = ["api.hip", "conv_gemm.hip", "conv_direct.hip", "layers.hip", "sma.hip", "test_hooks.hip",
+           "conv_static.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

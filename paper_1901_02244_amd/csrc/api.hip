@@ -549,6 +549,12 @@ namespace {
 
 std::string g_create_error;
 
+}  // namespace
+
+void cbk::note_error(const std::string& msg) { g_create_error = msg; }
+
+namespace {
+
 int fail(cb_ctx* c, int code, const std::string& msg) {
   if (c) c->err = msg;
   else g_create_error = msg;

@@ -9,7 +9,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace cbk {
+
+// Records the message that cb_last_error(NULL) returns (a failure of a call
+// made without a context).
+void note_error(const std::string& msg);
 
 // Per-launch timing.  When armed, the next kernel launch on this thread
 // passes the two events to hipExtLaunchKernel, which stamps them on the
