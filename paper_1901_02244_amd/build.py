@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libcrossbow_sma.so")
 SOURCES = ["api.hip", "conv_gemm.hip", "conv_direct.hip", "layers.hip", "sma.hip", "test_hooks.hip",
-           "conv_static.hip"]
+           "conv_static.hip", "lenet.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -79,6 +79,11 @@ struct Plan {
   int64_t P = 0, Pp = 0;
   int input = -1, logits = -1;
   bool loss_per_image = false;  // the loss buffer holds k*b per-image terms (fused head)
+  // The MNIST-shaped LeNet runs as two fused launches (lenet.hip) instead of
+  // the operator list; its scratch: per-image loss terms, conv gradient
+  // shares and FC vectors.
+  bool lenet_fused = false;
+  int64_t off_lenet_loss = -1, off_lenet_conv = -1, off_lenet_fc = -1;
   // workspace layout (bytes)
   int64_t off_W = 0, off_G = 0, off_Z = 0, off_Zp = 0, off_Wprev = -1;
   int64_t off_loss = 0, off_flag = 0, off_bnpart = 0;
@@ -283,6 +288,8 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p, int kcap = 0) {
   }
   if (!ok) return false;
   p.Pp = align_up(p.P, 64);
+  p.lenet_fused = m->arch == CB_ARCH_LENET5 &&
+                  lenet_fused_ok(m->in_c, m->in_h, m->in_w, m->num_classes);
 
   // backward routing: visit ops in reverse, track which gradients exist
   std::vector<char> written(p.t.size(), 0);
@@ -345,6 +352,17 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p, int kcap = 0) {
   p.off_Zp = take(p.Pp * 4);
   if (m->learner_momentum != 0.f) p.off_Wprev = take(kp);
   const int64_t N = (int64_t)k * b;
+  if (p.lenet_fused) {
+    for (Op& o : p.ops) o.splits = 1;
+    p.off_lenet_loss = take(N * 4);
+    p.off_lenet_conv = take(N * LENET_CONV_PARAMS * 4);
+    p.off_lenet_fc = take(N * LENET_FC_VEC * 4);
+    p.off_bnpart = take(16);
+    p.off_loss = take((int64_t)k * 4);
+    p.off_flag = take(16);
+    p.total = off;
+    return true;
+  }
   for (size_t i = 0; i < p.t.size(); ++i) {
     Tensor& x = p.t[i];
     const int64_t bytes = N * x.C * x.H * x.W * 4;
@@ -623,8 +641,39 @@ struct ProfScope {
     ps_.done(nm_, flops, bytes);               \
   } while (0)
 
+// The MNIST-shaped LeNet: one launch per image for the forward and
+// backward data path, one for the learners' gradients and losses.
+int enqueue_lenet(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s) {
+  const Plan& p = c->p;
+  LenetArgs a;
+  a.k = p.k; a.b = p.b; a.classes = p.m.num_classes;
+  a.x = x;
+  a.labels = labels;
+  a.w = c->W();
+  a.grad = c->G();
+  a.pstride = p.Pp;
+  a.loss = c->at<float>(p.off_lenet_loss);
+  a.learner_loss = c->at<float>(p.off_loss);
+  a.conv_part = c->at<float>(p.off_lenet_conv);
+  a.fc_vec = c->at<float>(p.off_lenet_fc);
+  const double N = (double)p.k * p.b, C = p.m.num_classes;
+  // multiply-adds per image: conv1 and conv2 forward, the FC layers forward
+  // and backward, conv2's data gradient, conv2's and conv1's weight shares
+  const double fc = 400.0 * 120 + 120.0 * 84 + 84.0 * C;
+  const double macs = 117600.0 + 240000.0 + 2.0 * fc + 240000.0 + 240000.0 + 117600.0;
+  const double img_bytes = 4.0 * (784.0 + 1 + (double)LENET_CONV_PARAMS + LENET_FC_VEC);
+  CB_LAUNCH(c, "lenet_image_k", 2.0 * macs * N, N * img_bytes + 4.0 * p.k * p.P,
+            lenet_image(a, s));
+  // the learners' FC weight gradients (sums over b images of outer products)
+  CB_LAUNCH(c, "lenet_learner_k", 2.0 * fc * N,
+            4.0 * (N * ((double)LENET_CONV_PARAMS + LENET_FC_VEC + 1) + p.k * (double)p.P + p.k),
+            lenet_learner(a, s));
+  return CB_OK;
+}
+
 int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s) {
   const Plan& p = c->p;
+  if (p.lenet_fused) return enqueue_lenet(c, x, labels, s);
   const int k = p.k, b = p.b, N = k * b;
   auto act = [&](int t) -> float* { return t == p.input ? const_cast<float*>(x) : c->at<float>(p.t[t].act); };
   auto grd = [&](int t) -> float* { return c->at<float>(p.t[t].grad); };
@@ -1034,20 +1083,27 @@ namespace {
 // The layers' split reductions, grouped: a group's reduction is launched on
 // the second stream right after the last of its weight gradients (in
 // backward order), so every group's but the last overlaps the rest of the
-// backward pass instead of waiting for its end.  From 128 input images of
+// backward pass instead of waiting for its end.  From 64 input images of
 // 32 x 32 per step (k*b*H*W input pixels), one group per layer: that
 // measured fastest (ResNet-32 k=4 b=32 2.6% and k=8..16 b=16 5% faster than
-// one reduction after the backward pass; ResNet-50 1.5%).  With less work
-// the weight gradients are short and the extra launches would crowd the
-// second stream (ResNet-32 k = 1..4 at b = 16 lost 5-15%), so all layers
-// form one group, reduced after the last weight gradient.
+// one reduction after the backward pass, k=4 and 6 at b=16 5-6%; ResNet-50
+// 1.5%).  With less work the weight gradients are short and the extra
+// launches would crowd the second stream (ResNet-32 k = 1 at b = 16 loses
+// 1.5%), so all layers form one group, reduced after the last weight
+// gradient.
 void build_split_tables(cb_ctx* c) {
   c->split_tables.clear();
   c->split_bytes.clear();
   c->split_after.clear();
+  if (c->p.lenet_fused) {  // no split partials on the fused LeNet path
+    c->split_per_layer = false;
+    c->first_conv = -1;
+    c->flush_at.assign(c->p.ops.size(), 0);
+    return;
+  }
   const int nops = (int)c->p.ops.size();
   const bool per_layer =
-      (int64_t)c->p.k * c->p.b * c->p.m.in_h * c->p.m.in_w >= (int64_t)128 * 32 * 32;
+      (int64_t)c->p.k * c->p.b * c->p.m.in_h * c->p.m.in_w >= (int64_t)64 * 32 * 32;
   c->split_per_layer = per_layer;
   c->first_conv = -1;
   for (int i = 0; i < nops && c->first_conv < 0; ++i)

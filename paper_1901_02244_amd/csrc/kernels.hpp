@@ -279,6 +279,33 @@ hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b
                         float* dlogits, float* loss, hipStream_t s,
                         const char** name = nullptr);
 
+// The MNIST-shaped LeNet (1 x 28 x 28 images) in two launches: one
+// workgroup per image for the forward pass, the loss and the backward data
+// path (lenet_image), then each learner's gradient and mean loss
+// (lenet_learner).
+constexpr int LENET_MAX_CLASSES = 64;
+constexpr int LENET_CONV_PARAMS = 150 + 6 + 2400 + 16;  // conv1 w, b, conv2 w, b
+// per image, the FC layers' inputs and output gradients:
+// p2 (400) | df1 (120) | f1 (120) | df2 (84) | f2 (84) | dlogits (<= 64)
+constexpr int LENET_DF1 = 400, LENET_F1 = 520, LENET_DF2 = 640, LENET_F2 = 724,
+              LENET_DL = 808, LENET_FC_VEC = 872;
+constexpr int LENET_LEARNER_BLOCKS = 260;  // ceil(P / 256) for up to 64 classes
+struct LenetArgs {
+  int k, b, classes;
+  const float* x;        // [k*b][1][28][28]
+  const int32_t* labels; // [k*b]
+  const float* w;        // replica 0 parameters (pstride apart)
+  float* grad;           // replica 0 gradient
+  int64_t pstride;
+  float* loss;           // per image [k*b]
+  float* learner_loss;   // per learner [k]: the mean over its b images
+  float* conv_part;      // [k*b][LENET_CONV_PARAMS]: each image's share of the conv gradients
+  float* fc_vec;         // [k*b][LENET_FC_VEC]
+};
+bool lenet_fused_ok(int in_c, int in_h, int in_w, int classes);
+hipError_t lenet_image(const LenetArgs& a, hipStream_t s);
+hipError_t lenet_learner(const LenetArgs& a, hipStream_t s);
+
 // Fused SMA synchronisation (Algorithm 1).  W, G, Wprev are [k][stride];
 // z, zp are [>= P] with P padded to a multiple of 4 elements.
 struct SMAArgs {

@@ -1,0 +1,412 @@
+// lenet.hip -- the learning task of the MNIST-shaped LeNet in two launches.
+//
+// LeNet on 28 x 28 single-channel images (Table 1's MNIST workload) is tiny:
+// one image's forward and backward pass is ~1 M multiply-adds, so the
+// operator-by-operator path spends its time in ~25 kernel boundaries per
+// iteration.  Here one workgroup per image keeps every activation of its
+// image in LDS and runs the whole forward pass, the loss (Eq. 2), the whole
+// backward data path and that image's share of the convolution weight
+// gradients (lenet_image_k); a second launch forms each learner's gradient:
+// the convolution shares summed over the learner's images in image order,
+// the FC weight gradients as sums over the images of outer products of the
+// stored FC inputs and output gradients, and the learner's mean loss
+// (lenet_learner_k).  The network is the one the library describes for
+// LeNet: conv 5x5x6 pad 2, ReLU, max 2x2/2, conv 5x5x16, ReLU, max 2x2/2,
+// FC 400-120 ReLU, FC 120-84 ReLU, FC 84-classes, softmax cross-entropy.
+// Max pooling takes the first strict maximum of its window in row-major
+// order; ReLU'(0) = 0.  Every sum runs in a fixed order (deterministic).
+#include "kernels.hpp"
+
+namespace cbk {
+namespace {
+
+constexpr int IMG = 28, PADW = 32;                 // input and its 2-pixel-padded copy
+constexpr int C1 = 6, A1 = IMG * IMG, P1W = 14, P1 = P1W * P1W;
+constexpr int C2 = 16, A2W = 10, A2 = A2W * A2W, P2W = 5, P2 = P2W * P2W;
+constexpr int F0 = C2 * P2, F1 = 120, F2 = 84;     // 400 -> 120 -> 84 -> classes
+constexpr int NW1 = C1 * 25, NW2 = C2 * C1 * 25;   // conv weights
+constexpr int THREADS = 512;
+constexpr int D2P = A2W + 8;          // padded da2 plane width (18)
+constexpr int R1PARTS = 7, R1ROWS = IMG / R1PARTS;  // conv1 weight shares: 7 slices of 4 rows
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// First strict maximum of a 2 x 2 window (row-major), its position 0..3.
+__device__ __forceinline__ int win_arg(float v0, float v1, float v2, float v3, float* best) {
+  int a = 0;
+  float b = v0;
+  if (v1 > b) { b = v1; a = 1; }
+  if (v2 > b) { b = v2; a = 2; }
+  if (v3 > b) { b = v3; a = 3; }
+  *best = b;
+  return a;
+}
+
+// FC weights pass through one LDS buffer: W1 (120 x 400) in three slabs of
+// 40 rows, W2 and W3 whole.  All threads copy a slab with 16-byte loads, so
+// the whole slab is in flight at once instead of each output's row being a
+// chain of dependent L2 round trips.
+constexpr int SLAB_ROWS = 40, SLAB = SLAB_ROWS * F0;  // 16000 floats (64 KB)
+static_assert(F2 * F1 <= SLAB && LENET_MAX_CLASSES * F2 <= SLAB, "FC weights fit the slab");
+
+// dst[0, n) = src[0, n); n a multiple of 4, src 16-byte aligned.
+__device__ __forceinline__ void stage(float* dst, const float* src, int n) {
+  const v4f* s4 = reinterpret_cast<const v4f*>(src);
+  v4f* d4 = reinterpret_cast<v4f*>(dst);
+  const int n4 = n >> 2;
+  int e = threadIdx.x;
+#pragma unroll 4
+  for (; e + 3 * THREADS < n4; e += 4 * THREADS) {
+    const v4f a0 = s4[e], a1 = s4[e + THREADS], a2 = s4[e + 2 * THREADS], a3 = s4[e + 3 * THREADS];
+    d4[e] = a0;
+    d4[e + THREADS] = a1;
+    d4[e + 2 * THREADS] = a2;
+    d4[e + 3 * THREADS] = a3;
+  }
+  for (; e < n4; e += THREADS) d4[e] = s4[e];
+}
+
+// y[o0 + r] = bias[o0 + r] + sum_i W[r][i] x[i] for the nrows rows of W in
+// LDS (row length nin), a wave per row, lanes over the inputs; ReLU if relu.
+__device__ __forceinline__ void fc_rows(const float* W, const float* bias, const float* x, int nin,
+                                        int o0, int nrows, bool relu, float* y) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int r = w; r < nrows; r += THREADS / 64) {
+    float s = 0.f;
+    for (int i = lane; i < nin; i += 64) s += W[r * nin + i] * x[i];
+    s = wave_sum(s) + bias[o0 + r];
+    if (lane == 0) y[o0 + r] = relu ? (s > 0.f ? s : 0.f) : s;
+  }
+}
+
+__global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
+  __shared__ float xs[PADW * PADW];
+  __shared__ float w1[NW1], b1[C1], w2[NW2], b2[C2];
+  __shared__ float a1[C1 * A1], p1[C1 * P1];
+  __shared__ float a2[C2 * A2], p2[F0];
+  __shared__ unsigned char g1[C1 * P1], g2[F0];
+  __shared__ float f1[F1], f2[F2], lg[LENET_MAX_CLASSES];
+  __shared__ float dl[LENET_MAX_CLASSES], df2[F2], df1[F1], dp2[F0];
+  __shared__ float da2[C2 * A2], dp1[C1 * P1];
+  __shared__ __attribute__((aligned(16))) float wb[SLAB];
+  // once the FC weights are done with, their buffer holds da2 with a
+  // 4-pixel zero border, the two halves of conv2's data gradient and the
+  // seven slices of conv1's weight shares
+  float* const da2p = wb;
+  float* const pdp1 = wb + C2 * D2P * D2P;
+  float* const part1 = pdp1 + 2 * C1 * P1;
+  static_assert(C2 * D2P * D2P + 2 * C1 * P1 + R1PARTS * (NW1 + C1) <= SLAB, "aliases fit");
+  const int tid = threadIdx.x;
+  const int n = blockIdx.x, j = n / a.b;  // image n belongs to learner j
+  const float* Wj = a.w + (int64_t)j * a.pstride;
+  const float* x = a.x + (int64_t)n * A1;
+  const int C = a.classes;
+  const float* fw1 = Wj + NW1 + C1 + NW2 + C2;
+  const float* fb1 = fw1 + F1 * F0;
+  const float* fw2 = fb1 + F1;
+  const float* fb2 = fw2 + F2 * F1;
+  const float* fw3 = fb2 + F2;
+  const float* fb3 = fw3 + C * F2;
+
+  // ---- forward -------------------------------------------------------
+  for (int e = tid; e < PADW * PADW; e += THREADS) {
+    const int r = e / PADW - 2, c = e % PADW - 2;
+    xs[e] = (r >= 0 && r < IMG && c >= 0 && c < IMG) ? x[r * IMG + c] : 0.f;
+  }
+  for (int e = tid; e < NW1 + C1 + NW2 + C2; e += THREADS) {
+    const float v = Wj[e];
+    if (e < NW1) w1[e] = v;
+    else if (e < NW1 + C1) b1[e - NW1] = v;
+    else if (e < NW1 + C1 + NW2) w2[e - NW1 - C1] = v;
+    else b2[e - NW1 - C1 - NW2] = v;
+  }
+  __syncthreads();
+  for (int pix = tid; pix < A1; pix += THREADS) {  // conv1 + bias + ReLU, a thread per pixel
+    const int y = pix / IMG, xx = pix % IMG;
+    float v[25];
+#pragma unroll
+    for (int t = 0; t < 25; ++t) v[t] = xs[(y + t / 5) * PADW + xx + t % 5];
+#pragma unroll
+    for (int co = 0; co < C1; ++co) {
+      float s = 0.f;
+#pragma unroll
+      for (int t = 0; t < 25; ++t) s += w1[co * 25 + t] * v[t];
+      s += b1[co];
+      a1[co * A1 + pix] = s > 0.f ? s : 0.f;
+    }
+  }
+  __syncthreads();
+  for (int o = tid; o < C1 * P1; o += THREADS) {  // max pool 2x2/2
+    const int c = o / P1, py = (o % P1) / P1W, px = o % P1W;
+    const float* v = a1 + c * A1 + 2 * py * IMG + 2 * px;
+    float b;
+    g1[o] = (unsigned char)win_arg(v[0], v[1], v[IMG], v[IMG + 1], &b);
+    p1[o] = b;
+  }
+  __syncthreads();
+  for (int t0 = tid; t0 < A2 * (C2 / 4); t0 += THREADS) {  // conv2 + bias + ReLU
+    const int pix = t0 % A2, cg = t0 / A2;  // a thread per pixel and 4 output channels
+    const int y = pix / A2W, xx = pix % A2W;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < C1; ++c) {
+      float v[25];
+#pragma unroll
+      for (int t = 0; t < 25; ++t) v[t] = p1[c * P1 + (y + t / 5) * P1W + xx + t % 5];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int t = 0; t < 25; ++t) acc[u] += w2[(cg * 4 + u) * 150 + c * 25 + t] * v[t];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float s = acc[u] + b2[cg * 4 + u];
+      a2[(cg * 4 + u) * A2 + pix] = s > 0.f ? s : 0.f;
+    }
+  }
+  __syncthreads();
+  for (int o = tid; o < F0; o += THREADS) {  // max pool 2x2/2
+    const int c = o / P2, py = (o % P2) / P2W, px = o % P2W;
+    const float* v = a2 + c * A2 + 2 * py * A2W + 2 * px;
+    float b;
+    g2[o] = (unsigned char)win_arg(v[0], v[1], v[A2W], v[A2W + 1], &b);
+    p2[o] = b;
+  }
+  __syncthreads();
+  for (int o0 = 0; o0 < F1; o0 += SLAB_ROWS) {  // FC1 + ReLU, by slabs
+    stage(wb, fw1 + o0 * F0, SLAB);
+    __syncthreads();
+    fc_rows(wb, fb1, p2, F0, o0, SLAB_ROWS, true, f1);
+    __syncthreads();
+  }
+  stage(wb, fw2, F2 * F1);  // FC2 + ReLU
+  __syncthreads();
+  fc_rows(wb, fb2, f1, F1, 0, F2, true, f2);
+  __syncthreads();
+  stage(wb, fw3, C * F2);  // FC3 (kept in LDS for its data gradient)
+  __syncthreads();
+  fc_rows(wb, fb3, f2, F2, 0, C, false, lg);
+  __syncthreads();
+  // softmax cross-entropy of this image: the loss term and (softmax -
+  // onehot) / b; a label out of range gives a NaN term and no one-hot
+  if (tid < 64) {
+    const int label = a.labels[n];
+    const bool on = tid < C;
+    const float o = on ? lg[tid] : -INFINITY;
+    const float mx = wave_max(o);
+    const float lse = mx + logf(wave_sum(on ? expf(o - mx) : 0.f));
+    const bool yok = (unsigned)label < (unsigned)C;
+    if (tid == 0) a.loss[n] = yok ? lse - lg[label] : NAN;
+    if (on) dl[tid] = (expf(o - lse) - (tid == label ? 1.f : 0.f)) / a.b;
+  }
+  __syncthreads();
+
+  // ---- backward ------------------------------------------------------
+  for (int i = tid; i < F2; i += THREADS) {
+    float s = 0.f;
+    for (int o = 0; o < C; ++o) s += dl[o] * wb[o * F2 + i];
+    df2[i] = f2[i] > 0.f ? s : 0.f;
+  }
+  __syncthreads();
+  stage(wb, fw2, F2 * F1);
+  __syncthreads();
+  for (int i = tid; i < F1; i += THREADS) {
+    float s = 0.f;
+    for (int o = 0; o < F2; ++o) s += df2[o] * wb[o * F1 + i];
+    df1[i] = f1[i] > 0.f ? s : 0.f;
+  }
+  for (int i = tid; i < F0; i += THREADS) dp2[i] = 0.f;
+  for (int o0 = 0; o0 < F1; o0 += SLAB_ROWS) {  // dp2 = W1^T df1, slab by slab in order
+    __syncthreads();
+    stage(wb, fw1 + o0 * F0, SLAB);
+    __syncthreads();
+    for (int i = tid; i < F0; i += THREADS) {
+      float s = dp2[i];
+      for (int r = 0; r < SLAB_ROWS; ++r) s += df1[o0 + r] * wb[r * F0 + i];
+      dp2[i] = s;
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < C2 * D2P * D2P; e += THREADS) {  // pool2 backward, ReLU mask
+    const int c = e / (D2P * D2P), y = (e % (D2P * D2P)) / D2P - 4, xx = e % D2P - 4;
+    float d = 0.f;
+    if (y >= 0 && y < A2W && xx >= 0 && xx < A2W) {
+      const int o = c * P2 + (y >> 1) * P2W + (xx >> 1), pos = (y & 1) * 2 + (xx & 1);
+      const int a = c * A2 + y * A2W + xx;
+      d = (g2[o] == pos && a2[a] > 0.f) ? dp2[o] : 0.f;
+      da2[a] = d;
+    }
+    da2p[e] = d;
+  }
+  __syncthreads();
+  // conv2 data gradient: dp1[c][iy][ix] = sum over co, r, q of
+  // da2[co][iy - r][ix - q] w2[co][c][r][q]; a thread per input pixel and half
+  // of the output channels, all six input channels; the halves summed in order
+  for (int t0 = tid; t0 < 2 * P1; t0 += THREADS) {
+    const int pix = t0 % P1, half = t0 / P1;
+    const int iy = pix / P1W + 4, ix = pix % P1W + 4;
+    float acc[C1] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int co = half * (C2 / 2); co < (half + 1) * (C2 / 2); ++co) {
+      float v[25];
+#pragma unroll
+      for (int t = 0; t < 25; ++t) v[t] = da2p[co * D2P * D2P + (iy - t / 5) * D2P + ix - t % 5];
+#pragma unroll
+      for (int c = 0; c < C1; ++c)
+#pragma unroll
+        for (int t = 0; t < 25; ++t) acc[c] += w2[co * 150 + c * 25 + t] * v[t];
+    }
+#pragma unroll
+    for (int c = 0; c < C1; ++c) pdp1[half * C1 * P1 + c * P1 + pix] = acc[c];
+  }
+  __syncthreads();
+  for (int e = tid; e < C1 * P1; e += THREADS) dp1[e] = pdp1[e] + pdp1[C1 * P1 + e];
+  __syncthreads();
+  for (int e = tid; e < C1 * A1; e += THREADS) {  // pool1 backward, ReLU mask (in a1)
+    const int c = e / A1, y = (e % A1) / IMG, xx = e % IMG;
+    const int o = c * P1 + (y >> 1) * P1W + (xx >> 1), pos = (y & 1) * 2 + (xx & 1);
+    a1[e] = (g1[o] == pos && a1[e] > 0.f) ? dp1[o] : 0.f;
+  }
+  __syncthreads();
+
+  // ---- this image's share of the convolution weight gradients ---------
+  float* cw = a.conv_part + (int64_t)n * LENET_CONV_PARAMS;
+  // conv2: dW[co][c][r][q] = sum over y, x of da2[co][y][x] p1[c][y+r][x+q];
+  // a thread per (co, c, r) computes the five q, row by row
+  for (int t = tid; t < C2 * C1 * 5 + C2; t += THREADS) {
+    if (t < C2 * C1 * 5) {
+      const int co = t / 30, c = (t % 30) / 5, r = t % 5;
+      float acc[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int y = 0; y < A2W; ++y) {
+        float d[A2W], pr[P1W];
+#pragma unroll
+        for (int xx = 0; xx < A2W; ++xx) d[xx] = da2[co * A2 + y * A2W + xx];
+#pragma unroll
+        for (int xx = 0; xx < P1W; ++xx) pr[xx] = p1[c * P1 + (y + r) * P1W + xx];
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+#pragma unroll
+          for (int xx = 0; xx < A2W; ++xx) acc[q] += d[xx] * pr[xx + q];
+      }
+#pragma unroll
+      for (int q = 0; q < 5; ++q) cw[NW1 + C1 + co * 150 + c * 25 + r * 5 + q] = acc[q];
+    } else {
+      const int co = t - C2 * C1 * 5;
+      float s = 0.f;
+      for (int e = 0; e < A2; ++e) s += da2[co * A2 + e];
+      cw[NW1 + C1 + NW2 + co] = s;
+    }
+  }
+  // conv1: dW[co][r][q] over 28 x 28 pixels, in seven slices of four rows
+  // summed in order; a thread per (slice, co, r) computes the five q
+  for (int t = tid; t < R1PARTS * (C1 * 5 + C1); t += THREADS) {
+    const int part = t / (C1 * 5 + C1), u = t % (C1 * 5 + C1);
+    const int y0 = part * R1ROWS;
+    if (u < C1 * 5) {
+      const int co = u / 5, r = u % 5;
+      float acc[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int y = y0; y < y0 + R1ROWS; ++y) {
+        float d[IMG], xr[PADW];
+#pragma unroll
+        for (int xx = 0; xx < IMG; ++xx) d[xx] = a1[co * A1 + y * IMG + xx];
+#pragma unroll
+        for (int xx = 0; xx < PADW; ++xx) xr[xx] = xs[(y + r) * PADW + xx];
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+#pragma unroll
+          for (int xx = 0; xx < IMG; ++xx) acc[q] += d[xx] * xr[xx + q];
+      }
+#pragma unroll
+      for (int q = 0; q < 5; ++q) part1[part * (NW1 + C1) + co * 25 + r * 5 + q] = acc[q];
+    } else {
+      const int co = u - C1 * 5;
+      float s = 0.f;
+      for (int e = y0 * IMG; e < (y0 + R1ROWS) * IMG; ++e) s += a1[co * A1 + e];
+      part1[part * (NW1 + C1) + NW1 + co] = s;
+    }
+  }
+  // the FC layers' inputs and output gradients, for their weight gradients
+  float* fv = a.fc_vec + (int64_t)n * LENET_FC_VEC;
+  for (int e = tid; e < LENET_FC_VEC; e += THREADS) {
+    float v = 0.f;
+    if (e < LENET_DF1) v = p2[e];
+    else if (e < LENET_F1) v = df1[e - LENET_DF1];
+    else if (e < LENET_DF2) v = f1[e - LENET_F1];
+    else if (e < LENET_F2) v = df2[e - LENET_DF2];
+    else if (e < LENET_DL) v = f2[e - LENET_F2];
+    else if (e - LENET_DL < C) v = dl[e - LENET_DL];
+    fv[e] = v;
+  }
+  __syncthreads();
+  for (int u = tid; u < NW1 + C1; u += THREADS) {
+    float s = part1[u];
+#pragma unroll
+    for (int part = 1; part < R1PARTS; ++part) s += part1[part * (NW1 + C1) + u];
+    cw[u] = s;
+  }
+}
+
+// Learner j's gradient: blockIdx.y = j; each thread several parameters.
+__global__ __launch_bounds__(256) void lenet_learner_k(LenetArgs a) {
+  const int j = blockIdx.y, C = a.classes;
+  const int64_t P = LENET_CONV_PARAMS + (int64_t)F1 * F0 + F1 + F2 * F1 + F2 + C * F2 + C;
+  float* g = a.grad + (int64_t)j * a.pstride;
+  const float* cw = a.conv_part + (int64_t)j * a.b * LENET_CONV_PARAMS;
+  const float* fv = a.fc_vec + (int64_t)j * a.b * LENET_FC_VEC;
+  const int64_t o_fw1 = LENET_CONV_PARAMS, o_fb1 = o_fw1 + F1 * F0, o_fw2 = o_fb1 + F1,
+                o_fb2 = o_fw2 + F2 * F1, o_fw3 = o_fb2 + F2, o_fb3 = o_fw3 + C * F2;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < P; e += (int64_t)gridDim.x * 256) {
+    // (one parameter per thread: the grid covers P)
+    float s = 0.f;
+    if (e < LENET_CONV_PARAMS) {
+      for (int i = 0; i < a.b; ++i) s += cw[(int64_t)i * LENET_CONV_PARAMS + e];
+    } else {
+      // dW[o][in] = sum over images of dy[o] * x[in]; db[o] = sum of dy[o]
+      int dyo, xo = -1;
+      if (e < o_fb1) { dyo = LENET_DF1 + (int)((e - o_fw1) / F0); xo = (int)((e - o_fw1) % F0); }
+      else if (e < o_fw2) { dyo = LENET_DF1 + (int)(e - o_fb1); }
+      else if (e < o_fb2) { dyo = LENET_DF2 + (int)((e - o_fw2) / F1); xo = LENET_F1 + (int)((e - o_fw2) % F1); }
+      else if (e < o_fw3) { dyo = LENET_DF2 + (int)(e - o_fb2); }
+      else if (e < o_fb3) { dyo = LENET_DL + (int)((e - o_fw3) / F2); xo = LENET_F2 + (int)((e - o_fw3) % F2); }
+      else { dyo = LENET_DL + (int)(e - o_fb3); }
+      for (int i = 0; i < a.b; ++i) {
+        const float* v = fv + (int64_t)i * LENET_FC_VEC;
+        s += xo >= 0 ? v[dyo] * v[xo] : v[dyo];
+      }
+    }
+    g[e] = s;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    double l = 0.0;
+    for (int i = 0; i < a.b; ++i) l += (double)a.loss[(int64_t)j * a.b + i];
+    a.learner_loss[j] = (float)(l / a.b);
+  }
+}
+
+}  // namespace
+
+bool lenet_fused_ok(int in_c, int in_h, int in_w, int classes) {
+  return in_c == 1 && in_h == IMG && in_w == IMG && classes >= 1 && classes <= LENET_MAX_CLASSES;
+}
+
+hipError_t lenet_image(const LenetArgs& a, hipStream_t s) {
+  if (!lenet_fused_ok(1, IMG, IMG, a.classes) || a.k < 1 || a.b < 1) return hipErrorInvalidValue;
+  klaunch(lenet_image_k, dim3((unsigned)(a.k * a.b)), dim3(THREADS), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t lenet_learner(const LenetArgs& a, hipStream_t s) {
+  if (!lenet_fused_ok(1, IMG, IMG, a.classes) || a.k < 1 || a.b < 1) return hipErrorInvalidValue;
+  klaunch(lenet_learner_k, dim3(LENET_LEARNER_BLOCKS, (unsigned)a.k), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace cbk

@@ -402,6 +402,18 @@ def test_lenet_k8_b16_thousand_iterations():
     assert err_gold <= bound
 
 
+def test_lenet_operator_path_16x20():
+    """LeNet on 16 x 20 images, which the fused 28 x 28 path does not take:
+    the operator-by-operator kernels (5x5 GEMM convolutions, max pools, FC
+    kernels, softmax cross-entropy) end to end for three iterations."""
+    p = Pair("lenet5", 1, 16, 20, 7, k=2, b=3, seed=6)
+    for t in range(3):
+        p.step(t)
+        p.check_grads(verbose=t == 0)
+        p.sync(verbose=True)
+    p.summary(f"z rel-L2 {p.z_error():.2e}")
+
+
 def test_lenet_learner_momentum_and_unsynced_steps():
     p = Pair("lenet5", 1, 28, 28, 10, k=3, b=5, mu_l=0.9, seed=5)
     p.step(0)
