@@ -87,6 +87,7 @@ struct Plan {
   // workspace layout (bytes)
   int64_t off_W = 0, off_G = 0, off_Z = 0, off_Zp = 0, off_Wprev = -1;
   int64_t off_loss = 0, off_flag = 0, off_bnpart = 0;
+  int64_t off_loss_mean = -1;  // with per-image terms: each replica's mean [k]
   int64_t total = 0;
 };
 
@@ -413,7 +414,7 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p, int kcap = 0) {
     Op& xe = p.ops[i + 2];
     if (gp.kind != OP_GAP || fc.kind != OP_CONV || xe.kind != OP_XENT) continue;
     if (fc.in != gp.out || xe.in != fc.out || fc.R != 1 || fc.H != 1 || fc.W != 1 || fc.relu ||
-        !fc.need_dx || !head_ok(gp.C, gp.H * gp.W, fc.Co) ||
+        !fc.bias || !fc.need_dx || !head_ok(gp.C, gp.H * gp.W, fc.Co) ||
         p.t[gp.out].consumers != 1 || p.t[fc.out].consumers != 1)
       continue;
     gp.head = fc.head = xe.head = true;
@@ -456,6 +457,7 @@ bool make_plan(const cb_model* m, int k, int b, Plan& p, int kcap = 0) {
     if (o.kind == OP_CONV && o.add_mode != ADD_NONE) o.add_buf = p.ops[o.add_buf].dres;
   p.off_bnpart = take(std::max<int64_t>(bnpart, 16));
   p.off_loss = take((int64_t)k * b * 4);
+  if (p.loss_per_image) p.off_loss_mean = take((int64_t)k * 4);
   p.off_flag = take(16);
   p.total = off;
   return true;
@@ -791,9 +793,15 @@ int enqueue_step(cb_ctx* c, const float* x, const int32_t* labels, hipStream_t s
     const double flops = 2.0 * N * o.Ho * o.Wo * o.Co * o.Ci * o.R * o.R;
     const double wn = (double)o.Co * o.Ci * o.R * o.R;
     const double xin = (double)N * o.Ci * o.H * o.W, yout = (double)N * o.Co * o.Ho * o.Wo;
-    if (o.bias)
-      CB_LAUNCH(c, "channel_sum_k", 0.0, 4.0 * yout,
-                channel_sum(grd(o.out), k, b, o.Co, o.Ho * o.Wo, G + o.b_off, p.Pp, ss));
+    if (o.bias) {
+      // the fused head's FC also reduces the per-image loss terms to each
+      // replica's mean loss
+      const bool terms = o.head && p.loss_per_image;
+      CB_LAUNCH(c, "channel_sum_k", 0.0, 4.0 * (yout + (terms ? N + k : 0)),
+                channel_sum(grd(o.out), k, b, o.Co, o.Ho * o.Wo, G + o.b_off, p.Pp, ss,
+                            terms ? c->at<float>(p.off_loss) : nullptr,
+                            terms ? c->at<float>(p.off_loss_mean) : nullptr));
+    }
     ConvBwdWeightArgs w;
     w.g = g;
     w.x = act(o.in);
@@ -1307,19 +1315,10 @@ int cb_get_grad(cb_ctx* c, int j, float* out_host, int64_t n) {
 int cb_get_loss(cb_ctx* c, float* out_host) {
   if (!c) return CB_EINVAL;
   const Plan& p = c->p;
-  if (!p.loss_per_image) return copy_out(c, c->at<float>(p.off_loss), out_host, p.k, p.k);
-  // per-image terms: each replica's mean in image order, in fp64
-  if (!out_host) return fail(c, CB_EINVAL, "output is NULL");
-  std::vector<float> terms((size_t)p.k * p.b);
-  const int rc = copy_out(c, c->at<float>(p.off_loss), terms.data(), (int64_t)terms.size(),
-                          (int64_t)terms.size());
-  if (rc) return rc;
-  for (int j = 0; j < p.k; ++j) {
-    double t = 0.0;
-    for (int n = 0; n < p.b; ++n) t += (double)terms[(size_t)j * p.b + n];
-    out_host[j] = (float)(t / p.b);
-  }
-  return CB_OK;
+  // with the fused head, the FC's bias-gradient kernel wrote each replica's
+  // mean of its per-image terms
+  const int64_t off = p.loss_per_image ? p.off_loss_mean : p.off_loss;
+  return copy_out(c, c->at<float>(off), out_host, p.k, p.k);
 }
 
 int cb_abi_version(void) { return CB_ABI_VERSION; }

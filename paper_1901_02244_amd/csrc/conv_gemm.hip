@@ -745,7 +745,8 @@ __global__ __launch_bounds__(256) void fc_dgrad_k(const float* dy, const float* 
 
 // db[j][c]: one block per (c, j), fixed-order reduction.
 __global__ __launch_bounds__(256) void channel_sum_k(const float* dy, int b, int C, int HW,
-                                                     float* db, int64_t pstride) {
+                                                     float* db, int64_t pstride,
+                                                     const float* terms, float* mean) {
   __shared__ float red[4];
   const int c = blockIdx.x, j = blockIdx.y;
   const int n = b * HW;
@@ -758,6 +759,12 @@ __global__ __launch_bounds__(256) void channel_sum_k(const float* dy, int b, int
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
   __syncthreads();
   if (threadIdx.x == 0) db[(int64_t)j * pstride + c] = (red[0] + red[1]) + (red[2] + red[3]);
+  if (terms && c == 0 && threadIdx.x == 0) {
+    // the replica's mean loss (Eq. 2) from its b per-image terms, in order
+    double t = 0.0;
+    for (int i = 0; i < b; ++i) t += (double)terms[(int64_t)j * b + i];
+    mean[j] = (float)(t / b);
+  }
 }
 
 inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
@@ -1015,8 +1022,8 @@ void split_table_add(SplitTable& t, const float* partial, float* dw, int64_t n, 
 }
 
 hipError_t channel_sum(const float* dy, int k, int b, int C, int HW, float* db, int64_t pstride,
-                       hipStream_t s) {
-  klaunch(channel_sum_k, dim3(C, k), dim3(256), 0, s, dy, b, C, HW, db, pstride);
+                       hipStream_t s, const float* terms, float* mean) {
+  klaunch(channel_sum_k, dim3(C, k), dim3(256), 0, s, dy, b, C, HW, db, pstride, terms, mean);
   return hipGetLastError();
 }
 

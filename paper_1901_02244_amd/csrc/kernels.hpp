@@ -182,8 +182,11 @@ constexpr int SMALL_SPLIT_SEGS = 4;
 void split_table_add(SplitTable& t, const float* partial, float* dw, int64_t n, int splits);
 hipError_t reduce_splits(const SplitTable& t, int k, hipStream_t s, const char** name = nullptr);
 // db[j][c] = sum over replica j's images and pixels of dy[n][c][p].
+// With terms (per-image loss terms [k*b]), also mean[j] = the mean of
+// replica j's b terms, summed in image order.
 hipError_t channel_sum(const float* dy, int k, int b, int C, int HW, float* db,
-                       int64_t pstride, hipStream_t s);
+                       int64_t pstride, hipStream_t s, const float* terms = nullptr,
+                       float* mean = nullptr);
 
 // Batch norm with per-replica batch statistics.
 enum { RES_NONE = 0, RES_SAME = 1, RES_SUBSAMPLE = 2 };
