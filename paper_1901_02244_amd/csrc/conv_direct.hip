@@ -140,8 +140,9 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
   const int T = a.k * per_rep;
   const int nchunk = a.Cin / CC;
 
-  // Tile t: replica, output-channel tile, then row tile (image-major), so
-  // the workgroups running together share filters and neighbouring rows.
+  // Tile t: replica, row tile (image-major), then output-channel tile, so
+  // that the tiles reading one input tile are numbered together and, with
+  // the XCD-major numbering below, fetch it into one XCD's L2.
   struct Tile {
     int j, co0, rt, img, oh0;
   };
@@ -149,8 +150,8 @@ __global__ __launch_bounds__(256) void conv3x3_k(DirectArgs a) {
     Tile d;
     d.j = t / per_rep;
     const int r = t - d.j * per_rep;
-    const int ct = r / rows_rep;
-    d.rt = r - ct * rows_rep;
+    d.rt = r / (a.Cout / BN);
+    const int ct = r - d.rt * (a.Cout / BN);
     d.co0 = ct * BN;
     d.img = d.rt / tiles_img;
     d.oh0 = (d.rt - d.img * tiles_img) * TH;
@@ -476,8 +477,8 @@ __global__ __launch_bounds__(256) void conv3x3s2_dgrad_k(DirectArgs a) {
     Tile d;
     d.j = t / per_rep;
     const int r = t - d.j * per_rep;
-    const int ct = r / rows_rep;
-    d.rt = r - ct * rows_rep;
+    d.rt = r / (a.Cout / BN);
+    const int ct = r - d.rt * (a.Cout / BN);
     d.co0 = ct * BN;  // first dX channel of the tile
     d.img = d.rt / tiles_img;
     d.m0 = (d.rt - d.img * tiles_img) * THO;
@@ -639,7 +640,7 @@ __global__ __launch_bounds__(256) void conv3x3s2_dgrad_k(DirectArgs a) {
   };
 
   const int G = gridDim.x;
-  int t = blockIdx.x;
+  int t = xcd_major(blockIdx.x, G);
   Tile d = decode(t);
   load(d, 0);
   store(0);
@@ -747,8 +748,15 @@ __global__ __launch_bounds__(256) void conv3x3_wgrad_k(WgradArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kq = lane >> 4, l16 = lane & 15;
   const int nci = a.Ci / 16;
-  const int co0 = (blockIdx.x / nci) * 16, ci0 = (blockIdx.x % nci) * 16;
-  const int split = blockIdx.y, j = blockIdx.z;
+  // The (co, ci) blocks of one replica and split read the same X and dY
+  // rows.  Workgroups reach the XCDs in turn, so the grid is renumbered
+  // XCD-major: such blocks share one XCD's L2 instead of fetching the rows
+  // into several.
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int lin = xcd_major(blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z), gx * gy * gridDim.z);
+  const int bx = lin % gx, rest = lin / gx;
+  const int co0 = (bx / nci) * 16, ci0 = (bx % nci) * 16;
+  const int split = rest % gy, j = rest / gy;
   const int H = a.H, HW = H * WW, tiles_img = H / TH;
   const int HI = H * ST, HWI = HI * WI;
   const int units = a.b * tiles_img;
