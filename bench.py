@@ -22,7 +22,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
-SWEEP_BEYOND = (48, 64, 96, 128)  # learner counts past the workload's sweep
+SWEEP_BEYOND = (48, 64, 96, 128, 192, 256)  # learner counts past the workload's sweep
 FP32_MFMA_PEAK_TFS = 157.3   # MI355X dense fp32 matrix
 
 
@@ -418,13 +418,16 @@ def cpu_baselines_by_config():
                                f"sync) in {dt:.1f} s, {where}"}
         log(f"[bench] cpu {name}: {out[name]['value']} images/s")
     sw = wl.RESNET32_SWEEP
-    dt, imgs = sma_run(sw, 1, k=32, learners=2)
-    out["resnet32_b16_k32"] = {
-        "value": round(imgs / dt, 2), "unit": "images/s", "cores": 1, "kind": "oracle",
-        "sample": f"one SMA iteration of 32 learners of 16: the gradients of 2 learners "
-                  f"({imgs} images) and the synchronisation of all 32 replicas, in {dt:.1f} s, "
-                  f"{where}; the other learners' gradients cost the same per image"}
-    log(f"[bench] cpu resnet32 k=32 b=16: {out['resnet32_b16_k32']['value']} images/s")
+    for k in sw.sweep_k:
+        n = min(k, 2)
+        dt, imgs = sma_run(sw, 1, k=k, learners=n)
+        key = f"resnet32_b16_k{k}"
+        out[key] = {
+            "value": round(imgs / dt, 2), "unit": "images/s", "cores": 1, "kind": "oracle",
+            "sample": f"one SMA iteration of {k} learner(s) of 16: the gradients of {n} "
+                      f"learner(s) ({imgs} images) and the synchronisation of all {k} replicas, "
+                      f"in {dt:.1f} s, {where}; every learner's gradient costs the same per image"}
+        log(f"[bench] cpu resnet32 k={k} b=16: {out[key]['value']} images/s")
     r50 = dataclasses.replace(wl.RESNET50_K2, b=2)
     dt, imgs = sma_run(r50, 1, k=2, learners=1)
     out["resnet50_k2_b32"] = {
@@ -531,7 +534,11 @@ def main():
     if not args.no_sweep:
         extra["sync_interval_sweep"] = sync_interval_sweep(wk)
         extra["ssgd_baseline_same_kernels"] = ssgd_baseline(wk)
-        extra["autotune_alg2_b16"] = autotune(wl.RESNET32_SWEEP)
+        extra["autotune_alg2_b16"] = at = autotune(wl.RESNET32_SWEEP)
+        if sweep:
+            top = max(v["images_per_s"] for v in sweep.values())
+            last = [t for _, t in at["trail_k_images_per_s"][-8:]]
+            at["last_8_mean_frac_of_sweep_max"] = round(sum(last) / len(last) / top, 4)
         extra["lenet_k8_b16"] = lenet_latency()
         extra["resnet50_k2_b32"] = resnet50_throughput()
     micro = None
