@@ -22,7 +22,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
-SWEEP_BEYOND = (48, 64, 96, 128, 192, 256)  # learner counts past the workload's sweep
+SWEEP_BEYOND = (48, 64, 96, 128, 192, 256, 384, 512)  # learner counts past the workload's sweep
 FP32_MFMA_PEAK_TFS = 157.3   # MI355X dense fp32 matrix
 
 
