@@ -248,32 +248,41 @@ def ssgd_baseline(wk, iters=100):
     return {"batch": one.b, "ms_per_step": round(ms, 4), "images_per_s": round(one.b / ms * 1e3, 1)}
 
 
-def lenet_latency(iters=200):
-    """LeNet-5, k = 8 learners of 16: launch/latency-bound; us per iteration
-    and kernel launches per iteration."""
+def lenet_latency(iters=1000, repeats=5):
+    """LeNet-5, k = 8 learners of 16 (and k = 2 learners of 4, 10 iterations):
+    launch/latency-bound; us per iteration (median of `repeats` runs) and
+    kernel launches per iteration."""
     import workloads as wl
 
     wk = wl.LENET_K8
-    ms, _, _, prof = time_training(wk, iters, 10, prof_steps=10)
+    ms, _, _, prof = time_training(wk, iters, 10, prof_steps=10, repeats=repeats)
     launches = sum(v[0] for v in prof.values())
     log(f"[bench] LeNet k=8 b=16: {ms * 1e3:.1f} us/iteration, {launches:.0f} launches/iteration")
+    small = wl.LENET_K2
+    ms2, _, _ = time_training(small, 10, 10, repeats=repeats)
+    log(f"[bench] LeNet k=2 b=4: {ms2 * 1e3:.1f} us/iteration")
     return {"us_per_iteration": round(ms * 1e3, 2), "launches_per_iteration": launches,
-            "images_per_s": round(wk.n_images / ms * 1e3, 1)}
+            "images_per_s": round(wk.n_images / ms * 1e3, 1), "iterations": iters,
+            "repeats": repeats,
+            "k2_b4": {"us_per_iteration": round(ms2 * 1e3, 2),
+                      "images_per_s": round(small.n_images / ms2 * 1e3, 1), "iterations": 10}}
 
 
-def resnet50_throughput(steps=5, warmup=2):
-    """ResNet-50, k = 2 learners of 32 images at 224 x 224: images/s."""
+def resnet50_throughput(steps=20, warmup=3, repeats=5):
+    """ResNet-50, k = 2 learners of 32 images at 224 x 224: images/s (median
+    of `repeats` runs of `steps` iterations)."""
     import workloads as wl
 
     wk = wl.RESNET50_K2
-    ms, _, _ = time_training(wk, steps, warmup, ring=2)
+    ms, _, _ = time_training(wk, steps, warmup, ring=2, repeats=repeats)
     log(f"[bench] ResNet-50 k=2 b=32: {ms:.2f} ms/iteration, {wk.n_images / ms * 1e3:.0f} images/s")
     return {"ms_per_iteration": round(ms, 3), "images_per_s": round(wk.n_images / ms * 1e3, 1),
-            "steps": steps}
+            "steps": steps, "repeats": repeats}
 
 
-def sma_micro(steps=20, warmup=3):
-    """Fused SMA kernel alone on ResNet-50's P with k = 32 replicas."""
+def sma_micro(steps=20, warmup=3, repeats=5):
+    """Fused SMA kernel alone on ResNet-50's P with k = 32 replicas (median
+    of `repeats` runs of `steps` launches)."""
     import torch
     import paper_1901_02244_amd as cb
     import workloads as wl
@@ -289,13 +298,16 @@ def sma_micro(steps=20, warmup=3):
     for _ in range(warmup):
         ctx.cb_sma_apply(g)
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record()
-    for _ in range(steps):
-        ctx.cb_sma_apply(g)
-    ev1.record()
-    torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / steps
+    runs = []
+    for _ in range(repeats):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(steps):
+            ctx.cb_sma_apply(g)
+        ev1.record()
+        torch.cuda.synchronize()
+        runs.append(ev0.elapsed_time(ev1) / steps)
+    ms = sorted(runs)[repeats // 2]
     nbytes = 4 * P * (3 * k + 4)
     ctx.cb_profile_enable(True)
     for _ in range(steps):
@@ -320,7 +332,7 @@ def sma_micro(steps=20, warmup=3):
     copy_gbs = 2 * half * 4 / (c0.elapsed_time(c1) / 5) / 1e6
     del src, dst
     torch.cuda.empty_cache()
-    return {"P": P, "k": k, "ms": round(ms, 4), "bytes": nbytes,
+    return {"P": P, "k": k, "ms": round(ms, 4), "runs_ms": [round(v, 4) for v in runs], "bytes": nbytes,
             "copy_GB/s": round(copy_gbs, 1), "frac_of_copy": round(nbytes / ms / 1e6 / copy_gbs, 4),
             "GB/s": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4),
             "kernel_avg_us": round(kms * 1e3 / la, 2),
@@ -454,7 +466,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--sweep-steps", type=int, default=100)
+    ap.add_argument("--sweep-steps", type=int, default=200)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-micro", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
@@ -525,10 +537,15 @@ def main():
     if not args.no_sweep:
         base = wl.RESNET32_SWEEP
         # the workload's k values, then larger ones until throughput stops rising
+        # (the workload's own k: 200 iterations, median of 5 runs; beyond it
+        # 50 iterations, median of 3, as each step there takes 5-50 ms)
         for k in base.sweep_k + SWEEP_BEYOND:
             w = base.with_k(k)
-            sms, swall, _ = time_training(w, args.sweep_steps, 3)
-            sweep[str(k)] = {"ms_per_step": round(sms, 4), "images_per_s": round(w.n_images / (sms / 1e3), 1)}
+            own = k in base.sweep_k
+            sms, swall, _ = time_training(w, args.sweep_steps if own else 50, 10 if own else 3,
+                                          repeats=5 if own else 3)
+            sweep[str(k)] = {"ms_per_step": round(sms, 4), "images_per_s": round(w.n_images / (sms / 1e3), 1),
+                             "runs_ms": [round(v, 4) for v in time_training.last_repeats]}
             log(f"[bench] sweep b=16 k={k}: {sms:.3f} ms/step, {w.n_images / (sms / 1e3):.0f} images/s")
     extra = {}
     if not args.no_sweep:

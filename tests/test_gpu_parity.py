@@ -573,10 +573,11 @@ def test_resnet32_k4_b32_hundred_iterations():
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("k", [32, 128])
+@pytest.mark.parametrize("k", [32, 128, 512])
 def test_resnet32_b16_full_size_learners(k):
-    """The largest points of the k sweep: 32 and 128 ResNet-32 learners of 16
-    images in every launch (other tile choices and grids than at k = 4).
+    """Points of the k sweep up to its largest: 32, 128 and 512 ResNet-32
+    learners of 16 images in every launch (other tile choices and grids than
+    at k = 4; at k = 512 every launch covers 8,192 images).
     The oracle recomputes the first, a middle and the last learner: loss and
     gradient at 1e-4 per tensor with ambiguous decisions resolved, and the
     synchronisation's update of those replicas (-lr times the gradient, all
