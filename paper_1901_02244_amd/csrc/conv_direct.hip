@@ -36,17 +36,6 @@ __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
 }
 __device__ __forceinline__ double shfl_xor_d(double v, int o) { return __shfl_xor(v, o, 64); }
 
-// Raw buffer reads: a wave-uniform descriptor over `bytes` bytes from base
-// and a 32-bit byte offset per lane.  An offset at or past `bytes` reads 0
-// (the buffer range check), which gives the tiles their zero border with
-// no branch: such lanes use OUTSIDE.
-constexpr uint32_t OUTSIDE = 0x80000000u;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const float* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, (int)bytes, 0x00020000);
-}
-__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t off_bytes) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off_bytes, 0, 0));
-}
 
 // Workgroups are handed to the eight XCDs in turn (workgroup w to XCD
 // w % 8).  Renumbering them XCD-major gives the workgroups of one XCD a

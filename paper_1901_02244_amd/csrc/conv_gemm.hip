@@ -65,7 +65,12 @@ __device__ __forceinline__ float relu0(float v) { return v > 0.f ? v : 0.f; }
 __device__ __forceinline__ double shfl_xor_d(double v, int o) { return __shfl_xor(v, o, 64); }
 
 // ---------------------------------------------------------------- forward
-template <int BM, int BN, int WM, int WN, int R, int BK>
+// CF (Ci a multiple of BK): the contraction runs over k = (r, s, ci) instead
+// of (ci, r, s), the same sum in another order (the same order for 1x1
+// filters).  A stage of BK steps then shares one tap (r, s), so its window
+// check and tap offset are computed once per stage, and a thread's steps
+// are consecutive channels (one plane apart in X, RS floats apart in W).
+template <int BM, int BN, int WM, int WN, int R, int BK, bool CF = false>
 __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   constexpr int RS = R * R;
   constexpr int LDK = BK + 4;
@@ -89,42 +94,89 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
 
   const int am = tid % BM;
   const int akq = __builtin_amdgcn_readfirstlane(tid / BM);
-  int ih0 = OUT_OF_RANGE, iw0 = OUT_OF_RANGE, xb = 0;
+  // The lane's output pixel: element offset of its window corner (ih0, iw0)
+  // and, as bit masks, the window rows and columns that lie inside the
+  // image (none past the last pixel).  Every load below is a buffer load
+  // whose offset is OUTSIDE where the element is zero, so the loaders have
+  // no branches.
+  int xb = 0;
+  uint32_t rmask = 0, cmask = 0;
   {
     const int m = m0 + am;
     if (m < M) {
       const int img = m / HoWo, p = m - img * HoWo, oh = p / g.Wo, ow = p - oh * g.Wo;
-      ih0 = oh * g.st - g.pad;
-      iw0 = ow * g.st - g.pad;
+      const int ih0 = oh * g.st - g.pad, iw0 = ow * g.st - g.pad;
       xb = img * g.Ci * HW + ih0 * g.W + iw0;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if ((unsigned)(ih0 + r) < (unsigned)g.H) rmask |= 1u << r;
+        if ((unsigned)(iw0 + r) < (unsigned)g.W) cmask |= 1u << r;
+      }
     }
   }
+  const uint32_t xbytes = (uint32_t)((int64_t)g.b * g.Ci * HW * 4);
+  const uint32_t wbytes = (uint32_t)((int64_t)N * K * 4);
+  // filter rows as 16-byte quads when every quad is aligned and whole
+  const bool wq = (K & 3) == 0 && (reinterpret_cast<uintptr_t>(a.w) & 15) == 0;
   float ra[KPT];
   float rb[BPT][4];
 
-  auto loadA = [&](int k0) {
+  auto loadA = [&](int k0, float (&ra)[KPT]) {
+    const auto xsrc = buf_rsrc_u(X, xbytes);
+    if constexpr (CF) {
+      const int rs = k0 / g.Ci, r = rs / R, s = rs - r * R;
+      const int c0 = k0 - rs * g.Ci + akq * KPT;  // wave-uniform
+      const uint32_t in = (rmask >> r) & (cmask >> s) & 1u;
+      const uint32_t a0 = in ? (uint32_t)(xb + c0 * HW + r * g.W + s) * 4u : OUTSIDE;
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) ra[i] = buf_ld(xsrc, a0 + (uint32_t)(i * HW) * 4u);
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int k = k0 + akq * KPT + i;  // wave-uniform
-      float v = 0.f;
-      if (k < K) {
-        const int ci = k / RS, rs = k - ci * RS, r = rs / R, s = rs - r * R;
-        if ((unsigned)(ih0 + r) < (unsigned)g.H && (unsigned)(iw0 + s) < (unsigned)g.W)
-          v = X[xb + ci * HW + r * g.W + s];
-      }
-      ra[i] = v;
+      const int ci = k / RS, rs = k - ci * RS, r = rs / R, s = rs - r * R;
+      const int koff = __builtin_amdgcn_readfirstlane(ci * HW + r * g.W + s);
+      const uint32_t in = (rmask >> r) & (cmask >> s) & (k < K ? 1u : 0u);
+      const uint32_t off = (uint32_t)(xb + koff) * 4u;
+      ra[i] = buf_ld(xsrc, (in & 1u) ? off : OUTSIDE);
     }
   };
-  auto loadB = [&](int k0) {
+  auto loadB = [&](int k0, float (&rb)[BPT][4]) {
+    const auto wsrc = buf_rsrc_u(Wt, wbytes);
+    if constexpr (CF) {
+      const int rs = k0 / g.Ci, c0 = k0 - rs * g.Ci;
+#pragma unroll
+      for (int u = 0; u < BPT; ++u) {
+        const int idx = tid + u * 256, n = n0 + idx / QPR, ci = c0 + 4 * (idx % QPR);
+        const uint32_t b0 = idx < BQ && n < N ? (uint32_t)(n * K + ci * RS + rs) * 4u : OUTSIDE;
+        if (RS == 1 && wq) {
+          const buf_v4f v = buf_ld4(wsrc, b0);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) rb[u][i] = v[i];
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) rb[u][i] = buf_ld(wsrc, b0 + 4u * i * RS);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < BPT; ++u) {
       const int idx = tid + u * 256, n = n0 + idx / QPR, kq = k0 + 4 * (idx % QPR);
+      const bool row = idx < BQ && n < N;
+      const uint32_t off = (uint32_t)(n * K + kq) * 4u;
+      if (wq) {
+        const buf_v4f v = buf_ld4(wsrc, row && kq < K ? off : OUTSIDE);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        rb[u][i] = (idx < BQ && n < N && kq + i < K) ? Wt[(int64_t)n * K + kq + i] : 0.f;
+        for (int i = 0; i < 4; ++i) rb[u][i] = v[i];
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rb[u][i] = buf_ld(wsrc, row && kq + i < K ? off + 4u * i : OUTSIDE);
+      }
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const float (&ra)[KPT], const float (&rb)[BPT][4]) {
 #pragma unroll
     for (int q = 0; q < KPT / 4; ++q)
       *reinterpret_cast<v4f*>(&As[buf][am * LDK + akq * KPT + 4 * q]) =
@@ -145,18 +197,18 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
     for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
   const int wm = wave % WM, wm0 = wm * TM * 16, wn0 = (wave / WM) * TN * 16;
   const int T = (K + BK - 1) / BK;
-  loadA(0);
-  loadB(0);
-  store(0);
+  loadA(0, ra);
+  loadB(0, rb);
+  store(0, ra, rb);
   __syncthreads();
   for (int t = 0; t < T; ++t) {
     const int cur = t & 1;
     if (t + 1 < T) {
-      loadA((t + 1) * BK);
-      loadB((t + 1) * BK);
+      loadA((t + 1) * BK, ra);
+      loadB((t + 1) * BK, rb);
     }
     mma_stage<TM, TN, BK>(As[cur], Bs[cur], wm0, wn0, lane, acc);
-    if (t + 1 < T) store(cur ^ 1);
+    if (t + 1 < T) store(cur ^ 1, ra, rb);
     __syncthreads();
   }
 
@@ -242,9 +294,12 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
 // MFMA work) and the epilogue writes the 2x2 block of each grid point: the
 // contraction at (2oh, 2ow), zero at the other three, every pixel through
 // the same accumulate / add / mask / batch-norm epilogue.
-template <int BM, int BN, int WM, int WN, int R, int ST, int BK, bool SP = false>
+// CF (stride 1 or the grid-only form, Co a multiple of BK): the contraction
+// runs over k = (r, s, co), tap-major as in the forward kernel.
+template <int BM, int BN, int WM, int WN, int R, int ST, int BK, bool SP = false, bool CF = false>
 __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   static_assert(!SP || (R == 1 && ST == 2), "the grid-only form is the 1x1 stride-2 case");
+  static_assert(!CF || ST == 1 || SP, "the tap-major loaders read dY at stride 1");
   constexpr int RS = R * R;
   constexpr int LDK = BK + 4;
   constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
@@ -285,8 +340,38 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   }
   float ra[KPT];
   float rb[BPT][4];
+  // tap-major loaders: the lane's dY window as row and column masks (tap
+  // (r, s) reads dY row thp - r, column twp - s), every load a buffer load
+  // that reads 0 at OUTSIDE
+  uint32_t rmask = 0, cmask = 0;
+  int ybase = 0;
+  if (CF && m0 + am < M) {
+    if (SP) {
+      rmask = cmask = 1u;
+      ybase = yb;
+    } else {
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if ((unsigned)(thp - r) < (unsigned)g.Ho) rmask |= 1u << r;
+        if ((unsigned)(twp - r) < (unsigned)g.Wo) cmask |= 1u << r;
+      }
+      ybase = yb + thp * g.Wo + twp;
+    }
+  }
+  const uint32_t dybytes = (uint32_t)((int64_t)g.b * g.Co * HoWo * 4);
+  const uint32_t wbytes = (uint32_t)((int64_t)g.Co * N * RS * 4);
 
-  auto loadA = [&](int k0) {
+  auto loadA = [&](int k0, float (&ra)[KPT]) {
+    if constexpr (CF) {
+      const auto ysrc = buf_rsrc_u(DY, dybytes);
+      const int rs = k0 / g.Co, r = rs / R, s = rs - r * R;
+      const int c0 = k0 - rs * g.Co + akq * KPT;  // wave-uniform
+      const uint32_t in = (rmask >> r) & (cmask >> s) & 1u;
+      const uint32_t a0 = in ? (uint32_t)(ybase + c0 * HoWo - r * g.Wo - s) * 4u : OUTSIDE;
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) ra[i] = buf_ld(ysrc, a0 + (uint32_t)(i * HoWo) * 4u);
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int k = k0 + akq * KPT + i;  // wave-uniform
@@ -308,7 +393,20 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       ra[i] = v;
     }
   };
-  auto loadB = [&](int k0) {
+  auto loadB = [&](int k0, float (&rb)[BPT][4]) {
+    if constexpr (CF) {
+      // W'[k][n] = W[co][n][r][s]: a quad is four consecutive co, N*RS apart
+      const auto wsrc = buf_rsrc_u(Wt, wbytes);
+      const int rs = k0 / g.Co, c0 = k0 - rs * g.Co;
+#pragma unroll
+      for (int u = 0; u < BPT; ++u) {
+        const int idx = tid + u * 256, n = n0 + idx / QPR, co = c0 + 4 * (idx % QPR);
+        const uint32_t b0 = idx < BQ && n < N ? (uint32_t)((co * N + n) * RS + rs) * 4u : OUTSIDE;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rb[u][i] = buf_ld(wsrc, b0 + (uint32_t)(i * N * RS) * 4u);
+      }
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < BPT; ++u) {
       const int idx = tid + u * 256, n = n0 + idx / QPR, kq = k0 + 4 * (idx % QPR);
@@ -321,7 +419,7 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       }
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const float (&ra)[KPT], const float (&rb)[BPT][4]) {
 #pragma unroll
     for (int q = 0; q < KPT / 4; ++q)
       *reinterpret_cast<v4f*>(&As[buf][am * LDK + akq * KPT + 4 * q]) =
@@ -342,18 +440,18 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
     for (int y = 0; y < TN; ++y) acc[x][y] = v4f{0.f, 0.f, 0.f, 0.f};
   const int wm0 = (wave % WM) * TM * 16, wn0 = (wave / WM) * TN * 16;
   const int T = (K + BK - 1) / BK;
-  loadA(0);
-  loadB(0);
-  store(0);
+  loadA(0, ra);
+  loadB(0, rb);
+  store(0, ra, rb);
   __syncthreads();
   for (int t = 0; t < T; ++t) {
     const int cur = t & 1;
     if (t + 1 < T) {
-      loadA((t + 1) * BK);
-      loadB((t + 1) * BK);
+      loadA((t + 1) * BK, ra);
+      loadB((t + 1) * BK, rb);
     }
     mma_stage<TM, TN, BK>(As[cur], Bs[cur], wm0, wn0, lane, acc);
-    if (t + 1 < T) store(cur ^ 1);
+    if (t + 1 < T) store(cur ^ 1, ra, rb);
     __syncthreads();
   }
 
@@ -792,6 +890,14 @@ hipError_t launch_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
   constexpr int BK = stage_k<BM>();
   const int M = a.g.b * a.g.Ho * a.g.Wo;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Co, BN), a.g.k);
+  if (a.g.Ci % BK == 0) {
+    klaunch((conv_fwd_k<BM, BN, WM, WN, R, BK, true>), grid, dim3(256), 0, s, a);
+    if (name) {
+      static const std::string n = std::string(tile_name<0, BM, BN, WM, WN, R, 0, BK>()) + " tap-major";
+      *name = n.c_str();
+    }
+    return hipGetLastError();
+  }
   klaunch((conv_fwd_k<BM, BN, WM, WN, R, BK>), grid, dim3(256), 0, s, a);
   if (name) *name = tile_name<0, BM, BN, WM, WN, R, 0, BK>();
   return hipGetLastError();
@@ -802,6 +908,18 @@ hipError_t launch_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char**
   constexpr int BK = stage_k<BM>();
   const int M = SP ? a.g.b * a.g.Ho * a.g.Wo : a.g.b * a.g.H * a.g.W;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Ci, BN), a.g.k);
+  if constexpr (ST == 1 || SP) {
+    if (a.g.Co % BK == 0) {
+      klaunch((conv_bwd_data_k<BM, BN, WM, WN, R, ST, BK, SP, true>), grid, dim3(256), 0, s, a);
+      if (name) {
+        static const std::string n =
+            std::string(SP ? tile_name<3, BM, BN, WM, WN, R, ST, BK>() : tile_name<1, BM, BN, WM, WN, R, ST, BK>()) +
+            " tap-major";
+        *name = n.c_str();
+      }
+      return hipGetLastError();
+    }
+  }
   klaunch((conv_bwd_data_k<BM, BN, WM, WN, R, ST, BK, SP>), grid, dim3(256), 0, s, a);
   if (name) *name = SP ? tile_name<3, BM, BN, WM, WN, R, ST, BK>() : tile_name<1, BM, BN, WM, WN, R, ST, BK>();
   return hipGetLastError();
@@ -824,13 +942,18 @@ constexpr int64_t MIN_WGS = 512;
 
 // Output-tile choice for the forward / data-gradient GEMM (M x N per
 // replica): the biggest tile of the N class that still yields MIN_WGS
-// workgroups over all replicas, else the smallest.  Returns 0..5:
+// workgroups over all replicas, else the smallest.  For N > 32 the
+// 128 x 64 tile is kept down to MIN_WGS / 4 workgroups: its waves hold
+// 64 x 32 outputs and read half the LDS bytes per MFMA of the 64 x 64
+// tile's 32 x 32, which at 3-4 workgroups per CU is the limit (ResNet-50
+// k=2 b=32: the 14 x 14 and 7 x 7 stages' 3 x 3 convolutions 325-375 ->
+// 210-250 us, the step 30.8 -> 29.3 ms).  Returns 0..5:
 //   0 (256,16)  1 (64,16)  2 (128,32)  3 (64,32)  4 (128,64)  5 (64,64)
 int pick_tile(int64_t M, int N, int k) {
   auto wgs = [&](int bm, int bn) { return (int64_t)cdiv(M, bm) * cdiv(N, bn) * k; };
   if (N <= 16) return wgs(256, 16) >= MIN_WGS ? 0 : 1;
   if (N <= 32) return wgs(128, 32) >= MIN_WGS ? 2 : 3;
-  if (wgs(128, 64) >= MIN_WGS) return 4;
+  if (wgs(128, 64) >= MIN_WGS / 4) return 4;
   // under one workgroup per CU even at 64 x 64: 16-column tiles (same rows)
   return wgs(64, 64) >= MIN_WGS / 2 ? 5 : 1;
 }

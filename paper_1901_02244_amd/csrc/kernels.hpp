@@ -39,6 +39,33 @@ inline void klaunch(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t shm, h
     hipLaunchKernelGGL(kernel, grid, block, shm, s, args...);
 }
 
+// Raw buffer reads: a wave-uniform descriptor over `bytes` bytes from base
+// and a 32-bit byte offset per lane.  An offset at or past `bytes` reads 0
+// (the buffer range check), which gives tiles their zero border, and
+// loaders their out-of-range elements, with no branch: such lanes use
+// OUTSIDE.  `bytes` must stay below 2 GiB.
+constexpr uint32_t OUTSIDE = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, (int)bytes, 0x00020000);
+}
+// The same descriptor from values the caller knows to be wave-uniform, moved
+// to scalar registers first, so that no load has to loop over lanes.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc_u(const float* base, uint32_t bytes) {
+  const uint64_t p = reinterpret_cast<uintptr_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  return buf_rsrc(reinterpret_cast<const float*>(((uint64_t)hi << 32) | lo),
+                  __builtin_amdgcn_readfirstlane(bytes));
+}
+__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t off_bytes) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off_bytes, 0, 0));
+}
+typedef float buf_v4f __attribute__((ext_vector_type(4)));
+// four consecutive floats; the whole quad reads 0 when it starts at or past `bytes`
+__device__ __forceinline__ buf_v4f buf_ld4(__amdgpu_buffer_rsrc_t r, uint32_t off_bytes) {
+  return __builtin_bit_cast(buf_v4f, __builtin_amdgcn_raw_buffer_load_b128(r, off_bytes, 0, 0));
+}
+
 // Geometry of one convolution layer (an FC layer is a 1x1 conv on a 1x1
 // image).  b = images per replica, k = replicas.
 struct ConvGeom {
