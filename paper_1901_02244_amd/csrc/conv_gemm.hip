@@ -498,9 +498,19 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       }
       if (SP) {
         // grid point m: dX rows 2oh and 2oh + 1, columns 2ow and 2ow + 1,
-        // two pixels (8 bytes) per row
-        for (int i = 0; i < 4 && mb + i < M; ++i) {
-          const int m = mb + i, im = m / HoWo, pp = m - im * HoWo, oh = pp / g.Wo, ow = pp - oh * g.Wo;
+        // two pixels (8 bytes) per row; the lane's four grid points are
+        // consecutive, so (image, oh, ow) is stepped rather than divided out
+        int im = mb / HoWo, pp = mb - im * HoWo, oh = pp / g.Wo, ow = pp - oh * g.Wo;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (mb + i >= M) break;
+          if (i > 0 && ++ow == g.Wo) {
+            ow = 0;
+            if (++oh == g.Ho) {
+              oh = 0;
+              ++im;
+            }
+          }
 #pragma unroll
           for (int r2 = 0; r2 < 2; ++r2) {
             const int ih = 2 * oh + r2;
