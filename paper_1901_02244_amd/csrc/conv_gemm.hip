@@ -476,6 +476,8 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
                           reinterpret_cast<uintptr_t>(BX) | reinterpret_cast<uintptr_t>(BY) |
                           (a.add_mode == ADD_SAME ? reinterpret_cast<uintptr_t>(ADD) : 0);
   const bool vec = (HW & 3) == 0 && (align & 15) == 0;
+  // grid-only form: four consecutive grid points share a grid row
+  const bool sp_vec = SP && (g.Wo & 3) == 0 && (align & 15) == 0;
   double s1[TN], s2[TN];
 #pragma unroll
   for (int y = 0; y < TN; ++y) s1[y] = s2[y] = 0.0;
@@ -495,6 +497,56 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       if (BG) {
         bg = BG[n];
         bb = BG[N + n];
+      }
+      if (SP && sp_vec) {
+        // the lane's four grid points (oh, ow .. ow + 3) lie in one grid row:
+        // dX rows 2oh and 2oh + 1, 8 consecutive pixels each from column
+        // 2ow, moved as two float4s per row.  Pixel 2ow + q of row 2oh holds
+        // the contraction of point q / 2 when q is even; every other pixel
+        // starts at 0.  The same epilogue as below, element for element.
+        const int im = mb / HoWo, pp = mb - im * HoWo, oh = pp / g.Wo, ow = pp - oh * g.Wo;
+#pragma unroll
+        for (int r2 = 0; r2 < 2; ++r2) {
+          const int ih = 2 * oh + r2;
+          const int64_t idx = (((int64_t)im * N + n) * g.H + ih) * g.W + 2 * ow;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int64_t e = idx + 4 * h;
+            v4f v = {r2 == 0 ? acc[x][y][2 * h] : 0.f, 0.f, r2 == 0 ? acc[x][y][2 * h + 1] : 0.f, 0.f};
+            if (a.accumulate) v += *reinterpret_cast<const v4f*>(DX + e);
+            if (a.add_mode == ADD_SAME) {
+              v += *reinterpret_cast<const v4f*>(ADD + e);
+            } else if (a.add_mode == ADD_SUBSAMPLE && ih % a.add_st == 0) {
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int iw = 2 * ow + 4 * h + q;
+                if (iw % a.add_st == 0)
+                  v[q] += ADD[(((int64_t)im * a.add_C + n) * Hs + ih / a.add_st) * Ws + iw / a.add_st];
+              }
+            }
+            if (MSK) {
+              const v4f mk = *reinterpret_cast<const v4f*>(MSK + e);
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                if (!(mk[q] > 0.f)) v[q] = 0.f;
+            }
+            *reinterpret_cast<v4f*>(DX + e) = v;
+            if (bn) {
+              const v4f bx = *reinterpret_cast<const v4f*>(BX + e);
+              v4f by = {1.f, 1.f, 1.f, 1.f};
+              if (BY) by = *reinterpret_cast<const v4f*>(BY + e);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const bool on = BY ? by[q] > 0.f : BG ? bn_affine(bx[q], bm, bi, bg, bb) > 0.f : true;
+                const float d = on ? v[q] : 0.f;
+                const float xh = (bx[q] - bm) * bi;
+                s1[y] += (double)d;
+                s2[y] += (double)d * xh;
+              }
+            }
+          }
+        }
+        continue;
       }
       if (SP) {
         // grid point m: dX rows 2oh and 2oh + 1, columns 2ow and 2ow + 1,
