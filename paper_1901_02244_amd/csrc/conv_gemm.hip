@@ -65,11 +65,13 @@ __device__ __forceinline__ float relu0(float v) { return v > 0.f ? v : 0.f; }
 __device__ __forceinline__ double shfl_xor_d(double v, int o) { return __shfl_xor(v, o, 64); }
 
 // ---------------------------------------------------------------- forward
-// CF (Ci a multiple of BK): the contraction runs over k = (r, s, ci) instead
-// of (ci, r, s), the same sum in another order (the same order for 1x1
-// filters).  A stage of BK steps then shares one tap (r, s), so its window
-// check and tap offset are computed once per stage, and a thread's steps
-// are consecutive channels (one plane apart in X, RS floats apart in W).
+// CF (Ci a multiple of BK): the contraction runs over k = (channel block of
+// BK, r, s, channel in the block) instead of (ci, r, s), the same sum in
+// another order (the same order for 1x1 filters).  A stage of BK steps then
+// shares one tap (r, s), so its window check and tap offset are computed
+// once per stage, and a thread's steps are consecutive channels (one plane
+// apart in X, RS floats apart in W); the R*R taps of a channel block follow
+// each other, so its planes stay in L2 across them.
 template <int BM, int BN, int WM, int WN, int R, int BK, bool CF = false>
 __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   constexpr int RS = R * R;
@@ -124,8 +126,8 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   auto loadA = [&](int k0, float (&ra)[KPT]) {
     const auto xsrc = buf_rsrc_u(X, xbytes);
     if constexpr (CF) {
-      const int rs = k0 / g.Ci, r = rs / R, s = rs - r * R;
-      const int c0 = k0 - rs * g.Ci + akq * KPT;  // wave-uniform
+      const int t = k0 / BK, blk = t / RS, rs = t - blk * RS, r = rs / R, s = rs - r * R;
+      const int c0 = blk * BK + akq * KPT;  // wave-uniform
       const uint32_t in = (rmask >> r) & (cmask >> s) & 1u;
       const uint32_t a0 = in ? (uint32_t)(xb + c0 * HW + r * g.W + s) * 4u : OUTSIDE;
 #pragma unroll
@@ -145,7 +147,7 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   auto loadB = [&](int k0, float (&rb)[BPT][4]) {
     const auto wsrc = buf_rsrc_u(Wt, wbytes);
     if constexpr (CF) {
-      const int rs = k0 / g.Ci, c0 = k0 - rs * g.Ci;
+      const int t = k0 / BK, blk = t / RS, rs = t - blk * RS, c0 = blk * BK;
 #pragma unroll
       for (int u = 0; u < BPT; ++u) {
         const int idx = tid + u * 256, n = n0 + idx / QPR, ci = c0 + 4 * (idx % QPR);
@@ -295,7 +297,8 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
 // contraction at (2oh, 2ow), zero at the other three, every pixel through
 // the same accumulate / add / mask / batch-norm epilogue.
 // CF (stride 1 or the grid-only form, Co a multiple of BK): the contraction
-// runs over k = (r, s, co), tap-major as in the forward kernel.
+// runs over k = (channel block, r, s, co in the block), as in the forward
+// kernel.
 template <int BM, int BN, int WM, int WN, int R, int ST, int BK, bool SP = false, bool CF = false>
 __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   static_assert(!SP || (R == 1 && ST == 2), "the grid-only form is the 1x1 stride-2 case");
@@ -364,8 +367,8 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
   auto loadA = [&](int k0, float (&ra)[KPT]) {
     if constexpr (CF) {
       const auto ysrc = buf_rsrc_u(DY, dybytes);
-      const int rs = k0 / g.Co, r = rs / R, s = rs - r * R;
-      const int c0 = k0 - rs * g.Co + akq * KPT;  // wave-uniform
+      const int t = k0 / BK, blk = t / RS, rs = t - blk * RS, r = rs / R, s = rs - r * R;
+      const int c0 = blk * BK + akq * KPT;  // wave-uniform
       const uint32_t in = (rmask >> r) & (cmask >> s) & 1u;
       const uint32_t a0 = in ? (uint32_t)(ybase + c0 * HoWo - r * g.Wo - s) * 4u : OUTSIDE;
 #pragma unroll
@@ -397,7 +400,7 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
     if constexpr (CF) {
       // W'[k][n] = W[co][n][r][s]: a quad is four consecutive co, N*RS apart
       const auto wsrc = buf_rsrc_u(Wt, wbytes);
-      const int rs = k0 / g.Co, c0 = k0 - rs * g.Co;
+      const int t = k0 / BK, blk = t / RS, rs = t - blk * RS, c0 = blk * BK;
 #pragma unroll
       for (int u = 0; u < BPT; ++u) {
         const int idx = tid + u * 256, n = n0 + idx / QPR, co = c0 + 4 * (idx % QPR);
