@@ -73,6 +73,13 @@ CONV = [
     ("ragged.1x1s2", 3, 2, 70, 9, 45, 1, 2, 0, 0, 0, 1),
     ("ragged.fc", 5, 3, 33, 1, 17, 1, 1, 0, 1, 1, 1),
     ("ragged.7x7s2", 2, 3, 3, 19, 5, 7, 2, 3, 0, 0, 0),
+    # ragged again with channel counts that take the tap-major GEMM loaders
+    # (channels a multiple of the stage depth), incl. the grid-only stride-2
+    # data gradient with and without its float4 epilogue
+    ("ragged.tap3x3", 3, 5, 32, 13, 48, 3, 1, 1, 1, 1, 1),
+    ("ragged.tap1x1", 2, 7, 64, 9, 80, 1, 1, 0, 0, 0, 1),
+    ("ragged.tap1x1s2", 2, 3, 64, 10, 96, 1, 2, 0, 0, 0, 1),
+    ("ragged.tap1x1s2v", 2, 3, 32, 16, 64, 1, 2, 0, 0, 0, 1),
 ]
 
 FULL_LIMIT = 6e8  # multiply-adds per replica below which the oracle does whole tensors
@@ -464,6 +471,13 @@ DGRAD_EPILOGUE = [
     ("direct.w8.mask.bn.rc", 2, 3, 64, 8, 64, 3, 1, 1, 0, 1, 0, 0, 1, 3),
     ("s2.w16.mask.bn.rc", 2, 4, 32, 16, 64, 3, 2, 1, 0, 1, 0, 0, 1, 3),
     ("gemm.5x5.mask.bn.rc", 2, 4, 6, 14, 16, 5, 1, 0, 0, 1, 0, 0, 1, 3),
+    # the tap-major GEMM loaders (output channels a multiple of the stage
+    # depth) under the full epilogue, and the grid-only stride-2 form with
+    # four grid points to a grid row (its float4 epilogue)
+    ("gemm.tap3x3.acc.mask.same.bn", 2, 3, 24, 13, 32, 3, 1, 1, 1, 1, 1, 24, 1, 1),
+    ("gemm.tap1x1.acc.mask.same.bn.rc", 2, 3, 24, 9, 64, 1, 1, 0, 1, 1, 1, 24, 1, 3),
+    ("gemm.1x1s2.grid4.acc.mask.same.bn", 2, 3, 24, 16, 64, 1, 2, 0, 1, 1, 1, 24, 1, 1),
+    ("gemm.1x1s2.grid4.sub.bn.relux", 2, 3, 24, 16, 64, 1, 2, 0, 0, 0, 2, 24, 1, 2),
 ]
 
 
