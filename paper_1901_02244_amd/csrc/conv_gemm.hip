@@ -906,6 +906,134 @@ __global__ __launch_bounds__(256) void fc_dgrad_k(const float* dy, const float* 
   dx[g] = s;
 }
 
+// Fully connected layers of at most 64 images per replica that the kernels
+// above do not take (wider layers): one workgroup per 16 outputs (forward)
+// or 16 inputs (data gradient) of a replica and all its images, on fp32
+// MFMA.  The 8 waves split the contraction into 8 ranges of whole 16-step
+// groups, and their partial tiles are summed in wave order through LDS.
+// The fragments come straight from memory: in each group a lane takes four
+// consecutive steps (16 bytes of an image row; the contraction length is a
+// multiple of 4, so the four are all in range or all out) and the matching
+// four weights.  Out-of-range reads use OUTSIDE and read 0.
+constexpr int FCM_WAVES = 8;
+
+template <int MF>
+__device__ __forceinline__ void fcm_reduce(v4f (&acc)[MF], v4f (*red)[MF][64], int wave,
+                                           int lane) {
+#pragma unroll
+  for (int f = 0; f < MF; ++f) red[wave][f][lane] = acc[f];
+  __syncthreads();
+  if (wave == 0)
+#pragma unroll
+    for (int f = 0; f < MF; ++f) {
+      v4f t = red[0][f][lane];
+      for (int q = 1; q < FCM_WAVES; ++q) t += red[q][f][lane];
+      acc[f] = t;
+    }
+}
+
+// Forward: y[n][co] = sum_ci x[n][ci] w[co][ci] (+ bias, ReLU); MF = image
+// fragments of 16.
+template <int MF>
+__global__ __launch_bounds__(64 * FCM_WAVES) void fc_fwd_mfma_k(const float* x, const float* w,
+                                                                const float* bias,
+                                                                int64_t pstride, int b, int Ci,
+                                                                int Co, int relu, float* y) {
+  __shared__ v4f red[FCM_WAVES][MF][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15;
+  const int q = (lane >> 4) * 4, j = blockIdx.y, co = blockIdx.x * 16 + l16;
+  const __amdgpu_buffer_rsrc_t xr = buf_rsrc_u(x + (int64_t)j * b * Ci, (uint32_t)(b * Ci) * 4u);
+  const __amdgpu_buffer_rsrc_t wr = buf_rsrc_u(w + (int64_t)j * pstride, (uint32_t)(Co * Ci) * 4u);
+  const int groups = (Ci + 15) / 16, per = (groups + FCM_WAVES - 1) / FCM_WAVES;
+  const int g0 = wave * per, g1 = min(groups, g0 + per);
+  v4f acc[MF];
+#pragma unroll
+  for (int f = 0; f < MF; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+  for (int g = g0; g < g1; ++g) {
+    const int k = g * 16 + q;  // the lane's first step
+    v4f av[MF];
+    float bv[4];
+#pragma unroll
+    for (int f = 0; f < MF; ++f) {
+      const int n = f * 16 + l16;
+      av[f] = buf_ld4(xr, (k < Ci && n < b) ? (uint32_t)(n * Ci + k) * 4u : OUTSIDE);
+    }
+    const uint32_t wo = (k < Ci && co < Co) ? (uint32_t)(co * Ci + k) * 4u : OUTSIDE;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) bv[kk] = buf_ld(wr, wo == OUTSIDE ? OUTSIDE : wo + 4u * kk);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int f = 0; f < MF; ++f) acc[f] = mfma4(av[f][kk], bv[kk], acc[f]);
+  }
+  fcm_reduce<MF>(acc, red, wave, lane);
+  if (wave != 0 || co >= Co) return;
+  const float bb = bias ? bias[(int64_t)j * pstride + co] : 0.f;
+#pragma unroll
+  for (int f = 0; f < MF; ++f)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int n = f * 16 + q + i;
+      if (n >= b) continue;
+      float v = acc[f][i] + bb;
+      if (relu) v = v > 0.f ? v : 0.f;
+      y[((int64_t)j * b + n) * Co + co] = v;
+    }
+}
+
+// Data gradient: dx[n][ci] = sum_co dy[n][co] w[co][ci], then accumulate
+// and the ReLU mask as in the GEMM epilogue.
+template <int MF>
+__global__ __launch_bounds__(64 * FCM_WAVES) void fc_dgrad_mfma_k(const float* dy, const float* w,
+                                                                  int64_t pstride, int b, int Ci,
+                                                                  int Co, int accumulate,
+                                                                  const float* mask, float* dx) {
+  __shared__ v4f red[FCM_WAVES][MF][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15;
+  const int q = (lane >> 4) * 4, j = blockIdx.y, ci = blockIdx.x * 16 + l16;
+  const __amdgpu_buffer_rsrc_t dr = buf_rsrc_u(dy + (int64_t)j * b * Co, (uint32_t)(b * Co) * 4u);
+  const __amdgpu_buffer_rsrc_t wr = buf_rsrc_u(w + (int64_t)j * pstride, (uint32_t)(Co * Ci) * 4u);
+  const int groups = (Co + 15) / 16, per = (groups + FCM_WAVES - 1) / FCM_WAVES;
+  const int g0 = wave * per, g1 = min(groups, g0 + per);
+  v4f acc[MF];
+#pragma unroll
+  for (int f = 0; f < MF; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+  for (int g = g0; g < g1; ++g) {
+    const int k = g * 16 + q;  // the lane's first output channel
+    v4f av[MF];
+    float bv[4];
+#pragma unroll
+    for (int f = 0; f < MF; ++f) {
+      const int n = f * 16 + l16;
+      av[f] = buf_ld4(dr, (k < Co && n < b) ? (uint32_t)(n * Co + k) * 4u : OUTSIDE);
+    }
+    const uint32_t wo = (k < Co && ci < Ci) ? (uint32_t)(k * Ci + ci) * 4u : OUTSIDE;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      bv[kk] = buf_ld(wr, wo == OUTSIDE ? OUTSIDE : wo + (uint32_t)(kk * Ci) * 4u);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int f = 0; f < MF; ++f) acc[f] = mfma4(av[f][kk], bv[kk], acc[f]);
+  }
+  fcm_reduce<MF>(acc, red, wave, lane);
+  if (wave != 0 || ci >= Ci) return;
+#pragma unroll
+  for (int f = 0; f < MF; ++f)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int n = f * 16 + q + i;
+      if (n >= b) continue;
+      const int64_t gi = ((int64_t)j * b + n) * Ci + ci;
+      float v = acc[f][i];
+      if (accumulate) v += dx[gi];
+      if (mask && !(mask[gi] > 0.f)) v = 0.f;
+      dx[gi] = v;
+    }
+}
+
 // db[j][c]: one block per (c, j), fixed-order reduction.
 __global__ __launch_bounds__(256) void channel_sum_k(const float* dy, int b, int C, int HW,
                                                      float* db, int64_t pstride,
@@ -1137,12 +1265,33 @@ bool fc_layer(const ConvGeom& g) {
   return g.R == 1 && g.S == 1 && g.H == 1 && g.W == 1 && g.st == 1 && g.pad == 0;
 }
 
+// The MFMA FC kernels: at most 64 images per replica, a contraction length
+// (klen) that is a multiple of 4, and every operand within the 32-bit byte
+// offsets of one buffer descriptor.
+bool fc_mfma_ok(const ConvGeom& g, int klen, int other) {
+  return fc_layer(g) && g.b >= 1 && g.b <= 64 && klen % 4 == 0 &&
+         (int64_t)klen * other * 4 < (int64_t)OUTSIDE && (int64_t)g.b * klen * 4 < (int64_t)OUTSIDE;
+}
+int fc_mfma_frags(int b) { return b <= 16 ? 1 : (b <= 32 ? 2 : 4); }
+
 hipError_t conv_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
   if (fc_layer(a.g) && !a.stats && a.g.Ci <= FC_MAX_K) {
     const int64_t outs = (int64_t)a.g.b * a.g.Co;
     klaunch(fc_fwd_k, dim3(cdiv(outs, 4), a.g.k), dim3(256), 0, s, a.x, a.w, a.bias, a.pstride,
             a.g.b, a.g.Ci, a.g.Co, a.relu, a.y);
     if (name) *name = "fc_fwd_k";
+    return hipGetLastError();
+  }
+  if (fc_mfma_ok(a.g, a.g.Ci, a.g.Co) && !a.stats && al16(a.x)) {
+    const dim3 grid(cdiv(a.g.Co, 16), a.g.k), block(64 * FCM_WAVES);
+    const int mf = fc_mfma_frags(a.g.b);
+    if (name) *name = mf == 1 ? "fc_fwd_mfma_k<1>" : mf == 2 ? "fc_fwd_mfma_k<2>" : "fc_fwd_mfma_k<4>";
+    if (mf == 1)
+      klaunch(fc_fwd_mfma_k<1>, grid, block, 0, s, a.x, a.w, a.bias, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.relu, a.y);
+    else if (mf == 2)
+      klaunch(fc_fwd_mfma_k<2>, grid, block, 0, s, a.x, a.w, a.bias, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.relu, a.y);
+    else
+      klaunch(fc_fwd_mfma_k<4>, grid, block, 0, s, a.x, a.w, a.bias, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.relu, a.y);
     return hipGetLastError();
   }
   // the direct kernel moves its outputs in 16-byte pieces (workspace
@@ -1162,6 +1311,19 @@ hipError_t conv_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** n
     klaunch(fc_dgrad_k, dim3(cdiv((int64_t)a.g.b * a.g.Ci, 256), a.g.k), dim3(256), 0, s, a.dy,
             a.w, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.accumulate, a.mask, a.dx);
     if (name) *name = "fc_dgrad_k";
+    return hipGetLastError();
+  }
+  if (fc_mfma_ok(a.g, a.g.Co, a.g.Ci) && !a.bn_part && a.add_mode == ADD_NONE && al16(a.dy)) {
+    const dim3 grid(cdiv(a.g.Ci, 16), a.g.k), block(64 * FCM_WAVES);
+    const int mf = fc_mfma_frags(a.g.b);
+    if (name)
+      *name = mf == 1 ? "fc_dgrad_mfma_k<1>" : mf == 2 ? "fc_dgrad_mfma_k<2>" : "fc_dgrad_mfma_k<4>";
+    if (mf == 1)
+      klaunch(fc_dgrad_mfma_k<1>, grid, block, 0, s, a.dy, a.w, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.accumulate, a.mask, a.dx);
+    else if (mf == 2)
+      klaunch(fc_dgrad_mfma_k<2>, grid, block, 0, s, a.dy, a.w, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.accumulate, a.mask, a.dx);
+    else
+      klaunch(fc_dgrad_mfma_k<4>, grid, block, 0, s, a.dy, a.w, a.pstride, a.g.b, a.g.Ci, a.g.Co, a.accumulate, a.mask, a.dx);
     return hipGetLastError();
   }
   const bool vec_ok = al16(a.dx) && al16(a.mask) && al16(a.bn_x) && al16(a.bn_y) && al16(a.add);

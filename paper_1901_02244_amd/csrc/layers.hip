@@ -422,6 +422,84 @@ __global__ __launch_bounds__(256) void maxpool_bwd_k(const float* dy, const int*
   dx[i] = s;
 }
 
+// The same two kernels over tiles of rows, through LDS: a workgroup stages
+// the rows its windows cover with coalesced reads, then visits the windows
+// there in the same order (identical results).  POOL_LDS floats of LDS.
+constexpr int POOL_LDS = 4096;
+
+// Forward: output rows [oh0, oh0 + toh) of plane blockIdx.x.
+__global__ __launch_bounds__(256) void maxpool_fwd_rows_k(const float* x, int H, int W, int K,
+                                                          int st, int pad, float* y, int Ho,
+                                                          int Wo, int* arg, int toh) {
+  __shared__ float xs[POOL_LDS];
+  const int64_t nc = blockIdx.x;
+  const int oh0 = blockIdx.y * toh, oh1 = min(Ho, oh0 + toh);
+  const int ih_lo = max(0, oh0 * st - pad), ih_hi = min(H, (oh1 - 1) * st - pad + K);
+  const float* xp = x + nc * H * W + ih_lo * W;
+  const int n = max(0, ih_hi - ih_lo) * W;
+  for (int e = threadIdx.x; e < n; e += 256) xs[e] = xp[e];
+  __syncthreads();
+  const int cells = (oh1 - oh0) * Wo;
+  for (int q = threadIdx.x; q < cells; q += 256) {
+    const int r0 = q / Wo, ow = q - r0 * Wo, oh = oh0 + r0;
+    int best = -1;
+    float bv = 0.f;
+    for (int r = 0; r < K; ++r) {
+      const int ih = oh * st - pad + r;
+      if (ih < 0 || ih >= H) continue;
+      for (int s = 0; s < K; ++s) {
+        const int iw = ow * st - pad + s;
+        if (iw < 0 || iw >= W) continue;
+        const float v = xs[(ih - ih_lo) * W + iw];
+        if (best < 0 || v > bv) {
+          best = ih * W + iw;
+          bv = v;
+        }
+      }
+    }
+    const int64_t o = (nc * Ho + oh) * Wo + ow;
+    y[o] = bv;
+    arg[o] = best;
+  }
+}
+
+// Backward: input rows [ih0, ih0 + tih) of plane blockIdx.x; the window rows
+// that can contain them are staged (gradient and argmax), half of the LDS
+// each.
+__global__ __launch_bounds__(256) void maxpool_bwd_rows_k(const float* dy, const int* arg,
+                                                          const float* x, int H, int W, int K,
+                                                          int st, int pad, int Ho, int Wo,
+                                                          float* dx, int mask_relu, int tih) {
+  __shared__ float ds[POOL_LDS / 2];
+  __shared__ int as[POOL_LDS / 2];
+  const int64_t nc = blockIdx.x;
+  const int ih0 = blockIdx.y * tih, ih1 = min(H, ih0 + tih);
+  const int oh_lo = max(0, (ih0 + pad - K + st) / st), oh_hi = min(Ho - 1, (ih1 - 1 + pad) / st);
+  const int n = max(0, oh_hi - oh_lo + 1) * Wo;
+  const int64_t ob = (nc * Ho + oh_lo) * Wo;
+  for (int e = threadIdx.x; e < n; e += 256) {
+    ds[e] = dy[ob + e];
+    as[e] = arg[ob + e];
+  }
+  __syncthreads();
+  const int cells = (ih1 - ih0) * W;
+  for (int q = threadIdx.x; q < cells; q += 256) {
+    const int r0 = q / W, iw = q - r0 * W, ih = ih0 + r0;
+    const int cell = ih * W + iw;
+    const int a_lo = max(0, (ih + pad - K + st) / st), a_hi = min(Ho - 1, (ih + pad) / st);
+    const int w_lo = max(0, (iw + pad - K + st) / st), w_hi = min(Wo - 1, (iw + pad) / st);
+    float s = 0.f;
+    for (int oh = a_lo; oh <= a_hi; ++oh)
+      for (int ow = w_lo; ow <= w_hi; ++ow) {
+        const int e = (oh - oh_lo) * Wo + ow;
+        if (as[e] == cell) s += ds[e];
+      }
+    const int64_t i = nc * H * W + cell;
+    if (mask_relu && !(x[i] > 0.f)) s = 0.f;
+    dx[i] = s;
+  }
+}
+
 // Global average pool: one wave per (image, channel) plane, lanes over its
 // pixels (coalesced), a fixed-order wave reduction.
 __global__ __launch_bounds__(256) void gap_fwd_k(const float* x, int64_t NC, int HW, float* y) {
@@ -453,42 +531,71 @@ __global__ __launch_bounds__(256) void gap_bwd_v4_k(const float* dy, int64_t n4,
 
 // One block per learner: mean over its b images of -log softmax(o)_y and
 // the gradient (softmax(o) - onehot(y)) / b (Eq. 2).
-// One block per learner; wave w takes rows w, w+4, ...  Each row's max
-// and sum of exponentials are wave reductions (no block barriers); the
-// waves' fp64 loss partials, each summed in row order, are combined in wave
-// order.
-__global__ __launch_bounds__(256) void softmax_xent_k(const float* logits, const int32_t* labels,
-                                                      int b, int classes, float* dlogits,
-                                                      float* loss) {
-  __shared__ double red[4];
+// 16 waves per learner; wave w takes rows w, w+16, ...  A row's logits are
+// read once into registers (lane l holds classes l, l+64, ...; up to
+// XENT_REG_CLASSES, beyond which the later passes read them again); its
+// max and sum of exponentials are wave reductions (no block barriers).  The
+// waves' fp64 loss partials, each summed in row order, are combined in
+// wave order.
+constexpr int XENT_WAVES = 16, XENT_CPL = 16, XENT_REG_CLASSES = 64 * XENT_CPL;
+__global__ __launch_bounds__(64 * XENT_WAVES) void softmax_xent_k(const float* logits,
+                                                                  const int32_t* labels, int b,
+                                                                  int classes, float* dlogits,
+                                                                  float* loss) {
+  __shared__ double red[XENT_WAVES];
   const int j = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const bool in_regs = classes <= XENT_REG_CLASSES;
   double tot = 0.0;
-  for (int i = w; i < b; i += 4) {
+  for (int i = w; i < b; i += XENT_WAVES) {
     const int64_t row = (int64_t)(j * b + i) * classes;
     const float* o = logits + row;
+    const int y = labels[j * b + i];
+    float v[XENT_CPL];
     float mx = -INFINITY;
-    for (int c = lane; c < classes; c += 64) mx = fmaxf(mx, o[c]);
+    if (in_regs) {
+#pragma unroll
+      for (int u = 0; u < XENT_CPL; ++u) {
+        const int c = lane + 64 * u;
+        v[u] = c < classes ? o[c] : -INFINITY;
+      }
+#pragma unroll
+      for (int u = 0; u < XENT_CPL; ++u) mx = fmaxf(mx, v[u]);
+    } else {
+      for (int c = lane; c < classes; c += 64) mx = fmaxf(mx, o[c]);
+    }
     mx = wave_max_f(mx);
     float se = 0.f;
-    for (int c = lane; c < classes; c += 64) se += expf(o[c] - mx);
+    if (in_regs) {
+#pragma unroll
+      for (int u = 0; u < XENT_CPL; ++u)
+        if (lane + 64 * u < classes) se += expf(v[u] - mx);
+    } else {
+      for (int c = lane; c < classes; c += 64) se += expf(o[c] - mx);
+    }
     se = wave_sum_f(se);
     const float lse = mx + logf(se);
-    const int y = labels[j * b + i];
     const bool yok = (unsigned)y < (unsigned)classes;
-    for (int c = lane; c < classes; c += 64)
-      dlogits[row + c] = (expf(o[c] - lse) - (c == y ? 1.f : 0.f)) / b;
+    if (in_regs) {
+#pragma unroll
+      for (int u = 0; u < XENT_CPL; ++u) {
+        const int c = lane + 64 * u;
+        if (c < classes) dlogits[row + c] = (expf(v[u] - lse) - (c == y ? 1.f : 0.f)) / b;
+      }
+    } else {
+      for (int c = lane; c < classes; c += 64)
+        dlogits[row + c] = (expf(o[c] - lse) - (c == y ? 1.f : 0.f)) / b;
+    }
     if (lane == 0) tot += yok ? (double)(lse - o[y]) : (double)NAN;
   }
   if (lane == 0) red[w] = tot;
   __syncthreads();
-  if (threadIdx.x == 0) loss[j] = (float)((((red[0] + red[1]) + red[2]) + red[3]) / b);
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int q = 0; q < XENT_WAVES; ++q) t += red[q];
+    loss[j] = (float)(t / b);
+  }
 }
 
-// Few classes: one row per thread (a wave per row would spend its time in
-// shuffles and serial latency).  Block j is replica j; rows beyond the block
-// size are taken in further passes.  The replica's loss is the fixed-order
-// sum of the per-row terms (thread order within a wave by xor butterfly,
-// then the four waves in order).
 constexpr int XENT_ROW_CLASSES = 32;
 __global__ __launch_bounds__(256) void softmax_xent_rows_k(const float* logits,
                                                            const int32_t* labels, int b,
@@ -696,6 +803,15 @@ hipError_t maxpool_fwd(const float* x, int N, int C, int H, int W, int K, int st
                        float* y, int Ho, int Wo, int* arg, hipStream_t s) {
   const int64_t n = (int64_t)N * C * Ho * Wo;
   if (n == 0) return hipSuccess;
+  // output rows per tile: as many as keep the input rows they cover within
+  // the LDS staging buffer, at most 16
+  const int room = POOL_LDS / W - K;
+  const int toh = room < 0 ? 0 : std::min(std::min(Ho, 16), room / st + 1);
+  if (toh >= 1) {
+    klaunch(maxpool_fwd_rows_k, dim3((unsigned)(N * C), cdiv(Ho, toh)), dim3(256), 0, s, x, H, W,
+            K, st, pad, y, Ho, Wo, arg, toh);
+    return hipGetLastError();
+  }
   klaunch(maxpool_fwd_k, dim3((unsigned)(N * C), cdiv((int64_t)Ho * Wo, 256)), dim3(256), 0, s, x, N * C, H, W, K, st,
                      pad, y, Ho, Wo, arg);
   return hipGetLastError();
@@ -706,6 +822,15 @@ hipError_t maxpool_bwd(const float* dy, const int* arg, const float* x, int N, i
                        hipStream_t s) {
   const int64_t n = (int64_t)N * C * H * W;
   if (n == 0) return hipSuccess;
+  // input rows per tile: at most 32, and the window rows they reach,
+  // (tih + K - 2) / st + 2 at most, within half the LDS staging buffer
+  int tih = std::min(H, 32);
+  while (tih >= 1 && ((tih + K - 2) / st + 2) * Wo > POOL_LDS / 2) --tih;
+  if (tih >= 1) {
+    klaunch(maxpool_bwd_rows_k, dim3((unsigned)(N * C), cdiv(H, tih)), dim3(256), 0, s, dy, arg, x,
+            H, W, K, st, pad, Ho, Wo, dx, mask_relu, tih);
+    return hipGetLastError();
+  }
   klaunch(maxpool_bwd_k, dim3((unsigned)(N * C), cdiv((int64_t)H * W, 256)), dim3(256), 0, s, dy, arg, x, N * C, H, W,
                      K, st, pad, Ho, Wo, dx, mask_relu);
   return hipGetLastError();
@@ -738,7 +863,8 @@ hipError_t softmax_xent(const float* logits, const int32_t* labels, int k, int b
             loss);
   } else {
     if (name) *name = "softmax_xent_k";
-    klaunch(softmax_xent_k, dim3(k), dim3(256), 0, s, logits, labels, b, classes, dlogits, loss);
+    klaunch(softmax_xent_k, dim3(k), dim3(64 * XENT_WAVES), 0, s, logits, labels, b, classes, dlogits,
+            loss);
   }
   return hipGetLastError();
 }

@@ -72,6 +72,11 @@ CONV = [
     ("ragged.5x5", 2, 3, 5, 11, 37, 5, 1, 2, 1, 1, 1),
     ("ragged.1x1s2", 3, 2, 70, 9, 45, 1, 2, 0, 0, 0, 1),
     ("ragged.fc", 5, 3, 33, 1, 17, 1, 1, 0, 1, 1, 1),
+    # FC layers too wide for the one-wave FC kernels (the MFMA FC kernels),
+    # with 1, 2 and 4 fragments of 16 images and ragged tiles
+    ("ragged.fc.b9", 2, 9, 1028, 1, 264, 1, 1, 0, 0, 1, 1),
+    ("ragged.fc.wide", 3, 21, 1100, 1, 300, 1, 1, 0, 1, 1, 1),
+    ("ragged.fc.b50", 2, 50, 1040, 1, 260, 1, 1, 0, 0, 0, 1),
     ("ragged.7x7s2", 2, 3, 3, 19, 5, 7, 2, 3, 0, 0, 0),
     # ragged again with channel counts that take the tap-major GEMM loaders
     # (channels a multiple of the stage depth), incl. the grid-only stride-2
@@ -309,32 +314,37 @@ def test_batchnorm_backward_relu_mask_from_x(case):
         assert max_rel(g[j * pstride + C:j * pstride + 2 * C], dbo) <= TOL_STEP1, (name, j, "dbeta")
 
 
-# (name, N, C, H, K, stride, pad, mask_relu)
+# (name, N, C, H, W, K, stride, pad, mask_relu)
 POOL = [
-    ("lenet.pool1", 128, 6, 28, 2, 2, 0, 1),
-    ("lenet.pool2", 128, 16, 10, 2, 2, 0, 1),
-    ("r50.pool", 64, 64, 112, 3, 2, 1, 0),
-    ("ragged", 3, 5, 11, 3, 2, 1, 1),
+    ("lenet.pool1", 128, 6, 28, 28, 2, 2, 0, 1),
+    ("lenet.pool2", 128, 16, 10, 10, 2, 2, 0, 1),
+    ("r50.pool", 64, 64, 112, 112, 3, 2, 1, 0),
+    ("ragged", 3, 5, 11, 11, 3, 2, 1, 1),
+    # rows too wide for the LDS tiles: the forward falls back to one thread
+    # per window; the backward takes one input row per tile ...
+    ("wide.rows1", 1, 2, 9, 1400, 3, 2, 1, 0),
+    # ... or, wider still, falls back to one thread per input cell
+    ("wide.fallback", 1, 2, 6, 4200, 3, 2, 1, 1),
 ]
 
 
 @pytest.mark.parametrize("case", POOL, ids=[c[0] for c in POOL])
 def test_maxpool_kernels(case):
-    name, N, C, H, K, st, pad, mask = case
+    name, N, C, H, W, K, st, pad, mask = case
     rng = _rng("pool" + name)
-    x = rng.standard_normal((N, C, H, H), dtype=np.float32)
+    x = rng.standard_normal((N, C, H, W), dtype=np.float32)
     if mask:
         x = np.maximum(x, 0)  # a ReLU output, with its many zero ties
-    Ho = (H + 2 * pad - K) // st + 1
-    dy = rng.standard_normal((N, C, Ho, Ho), dtype=np.float32)
+    Ho, Wo = (H + 2 * pad - K) // st + 1, (W + 2 * pad - K) // st + 1
+    dy = rng.standard_normal((N, C, Ho, Wo), dtype=np.float32)
     yo, dxo = oracle.maxpool(x, K, st, pad, dy=dy)
     if mask:
         dxo = np.where(x > 0, dxo, 0.0)
     xd, dyd = _dev(x), _dev(dy)
-    yd = torch.empty((N, C, Ho, Ho), dtype=torch.float32, device="cuda")
+    yd = torch.empty((N, C, Ho, Wo), dtype=torch.float32, device="cuda")
     dxd = torch.empty_like(xd)
-    arg = torch.empty((N, C, Ho, Ho), dtype=torch.int32, device="cuda")
-    assert cb.lib().cb_test_maxpool(N, C, H, H, K, st, pad, xd.data_ptr(), yd.data_ptr(),
+    arg = torch.empty((N, C, Ho, Wo), dtype=torch.int32, device="cuda")
+    assert cb.lib().cb_test_maxpool(N, C, H, W, K, st, pad, xd.data_ptr(), yd.data_ptr(),
                                     dyd.data_ptr(), dxd.data_ptr(), mask, arg.data_ptr(),
                                     torch.cuda.current_stream().cuda_stream) == 0
     torch.cuda.synchronize()
@@ -345,7 +355,9 @@ def test_maxpool_kernels(case):
 # (name, k, b, classes)
 XENT = [("lenet", 8, 16, 10), ("r32", 4, 32, 10), ("r50", 2, 32, 1000), ("ragged", 3, 5, 7),
         # a row per thread up to 32 classes, in several passes beyond 256 rows; a wave per row above
-        ("rows.b300", 2, 300, 10), ("rows.c32", 3, 7, 32), ("waves.c33", 2, 5, 33)]
+        ("rows.b300", 2, 300, 10), ("rows.c32", 3, 7, 32), ("waves.c33", 2, 5, 33),
+        # beyond 1024 classes a row is read again in each pass instead of kept in registers
+        ("waves.c1100", 2, 37, 1100)]
 
 
 @pytest.mark.parametrize("case", XENT, ids=[c[0] for c in XENT])
