@@ -37,15 +37,6 @@ __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
 __device__ __forceinline__ double shfl_xor_d(double v, int o) { return __shfl_xor(v, o, 64); }
 
 
-// Workgroups are handed to the eight XCDs in turn (workgroup w to XCD
-// w % 8).  Renumbering them XCD-major gives the workgroups of one XCD a
-// contiguous range of ids, so the neighbouring tiles they take share halo
-// rows and filters in that XCD's L2.  A bijection on [0, G) for any G.
-constexpr int NXCD = 8;
-__device__ __forceinline__ int xcd_major(int w, int G) {
-  const int x = w % NXCD, i = w / NXCD, q = G / NXCD, r = G % NXCD;
-  return x * q + min(x, r) + i;
-}
 
 // Channel stride of the LDS input tile, rounded so that the four lane groups
 // of a wave fall in distinct 16-bank ranges.

@@ -36,6 +36,24 @@ __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// The GEMM grids (x: M tiles, y: N tiles, z: replica, or replica and
+// split) renumbered XCD-major with the N tiles fastest: the tiles of one M
+// tile, which read the same rows of the left operand, and then the
+// neighbouring M tiles of the same z run on one XCD and share its L2.
+struct GemmTile {
+  int mt, nt, z;
+};
+__device__ __forceinline__ GemmTile gemm_tile() {
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int t = xcd_major(blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z), gx * gy * gridDim.z);
+  GemmTile r;
+  r.nt = t % gy;
+  const int rest = t / gy;
+  r.mt = rest % gx;
+  r.z = rest / gx;
+  return r;
+}
+
 // One LDS stage: As[rows][BK+4], Bs[cols][BK+4], both k-contiguous.
 template <int TM, int TN, int BK>
 __device__ __forceinline__ void mma_stage(const float* As, const float* Bs, int wm0, int wn0,
@@ -87,10 +105,11 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
 
   const ConvGeom g = a.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int j = blockIdx.z;
+  const GemmTile tl = gemm_tile();
+  const int j = tl.z;
   const int HW = g.H * g.W, HoWo = g.Ho * g.Wo;
   const int M = g.b * HoWo, N = g.Co, K = g.Ci * RS;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int m0 = tl.mt * BM, n0 = tl.nt * BN;
   const float* X = a.x + (int64_t)j * g.b * g.Ci * HW;
   const float* Wt = a.w + (int64_t)j * a.pstride;
 
@@ -262,7 +281,7 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
   // Per-channel partial sums of this tile for the batch norm that follows:
   // lanes with the same column combine by an xor butterfly, then the WM
   // waves of a column strip in wave order.  Written to
-  // stats[j][n][blockIdx.x][0..1].
+  // stats[j][n][M tile][0..1].
   __shared__ double red[WM][BN][2];
 #pragma unroll
   for (int y = 0; y < TN; ++y) {
@@ -284,7 +303,7 @@ __global__ __launch_bounds__(256) void conv_fwd_k(ConvFwdArgs a) {
       u += red[w][tid][0];
       v += red[w][tid][1];
     }
-    double* o = a.stats + (((int64_t)j * N + n0 + tid) * gridDim.x + blockIdx.x) * 2;
+    double* o = a.stats + (((int64_t)j * N + n0 + tid) * gridDim.x + tl.mt) * 2;
     o[0] = u;
     o[1] = v;
   }
@@ -316,10 +335,11 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
 
   const ConvGeom g = a.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int j = blockIdx.z;
+  const GemmTile tl = gemm_tile();
+  const int j = tl.z;
   const int HW = g.H * g.W, HoWo = g.Ho * g.Wo;
   const int M = SP ? g.b * HoWo : g.b * HW, N = g.Ci, K = g.Co * RS;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int m0 = tl.mt * BM, n0 = tl.nt * BN;
   const float* DY = a.dy + (int64_t)j * g.b * g.Co * HoWo;
   const float* Wt = a.w + (int64_t)j * a.pstride;
 
@@ -697,7 +717,7 @@ __global__ __launch_bounds__(256) void conv_bwd_data_k(ConvBwdDataArgs a) {
       u += red[q][tid][0];
       w += red[q][tid][1];
     }
-    double* o = a.bn_part + (((int64_t)j * N + n0 + tid) * gridDim.x + blockIdx.x) * 2;
+    double* o = a.bn_part + (((int64_t)j * N + n0 + tid) * gridDim.x + tl.mt) * 2;
     o[0] = u;
     o[1] = w;
   }
@@ -719,11 +739,12 @@ __global__ __launch_bounds__(256) void conv_bwd_weight_k(ConvBwdWeightArgs a) {
 
   const ConvGeom g = a.g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int j = blockIdx.z / a.splits, split = blockIdx.z - j * a.splits;
+  const GemmTile tl = gemm_tile();
+  const int j = tl.z / a.splits, split = tl.z - j * a.splits;
   const int HW = g.H * g.W, HoWo = g.Ho * g.Wo;
   const int Mo = g.Co, No = g.Ci * RS, L = g.b * HoWo;
   const int L0 = split * a.chunk, L1 = min(L, L0 + a.chunk);
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int m0 = tl.mt * BM, n0 = tl.nt * BN;
   const float* X = a.x + (int64_t)j * g.b * g.Ci * HW;
   const float* DY = a.dy + (int64_t)j * g.b * g.Co * HoWo;
 

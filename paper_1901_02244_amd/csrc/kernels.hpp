@@ -66,6 +66,16 @@ __device__ __forceinline__ buf_v4f buf_ld4(__amdgpu_buffer_rsrc_t r, uint32_t of
   return __builtin_bit_cast(buf_v4f, __builtin_amdgcn_raw_buffer_load_b128(r, off_bytes, 0, 0));
 }
 
+// Workgroups are handed to the eight XCDs in turn (workgroup w to XCD
+// w % 8).  Renumbering them XCD-major gives the workgroups of one XCD a
+// contiguous range of ids, so the neighbouring tiles they take share halo
+// rows and filters in that XCD's L2.  A bijection on [0, G) for any G.
+constexpr int NXCD = 8;
+__device__ __forceinline__ int xcd_major(int w, int G) {
+  const int x = w % NXCD, i = w / NXCD, q = G / NXCD, r = G % NXCD;
+  return x * q + min(x, r) + i;
+}
+
 // Geometry of one convolution layer (an FC layer is a 1x1 conv on a 1x1
 // image).  b = images per replica, k = replicas.
 struct ConvGeom {
