@@ -1095,19 +1095,20 @@ const char* tile_name() {
   return n.c_str();
 }
 
-// LDS stage depth: 32 contraction steps, 16 for 256-row tiles and for the
-// 128-row tiles of 1x1 convolutions and 3x3 data gradients.  The shallow
-// stage halves the LDS of a 128 x 64 tile (32 KB), so five workgroups share
-// a CU instead of two, and one workgroup's epilogue traffic overlaps the
-// others' MFMAs (ResNet-50 k=2 b=32: 1x1 data gradients 147 -> 130 us,
-// 1x1 forward 104 -> 96 us, 3x3 data gradients 252 -> 228 us; the 3x3
-// forward and the 1x1 stride-2 grid-only data gradient measured slower).
-template <int BM, int R, bool BWD, bool SP = false>
-constexpr int stage_k() { return BM >= 256 || (BM >= 128 && !SP && (R == 1 || BWD)) ? 16 : 32; }
+// LDS stage depth: 32 contraction steps, 16 for tiles of 128 rows or more
+// (the 1x1 stride-2 grid-only data gradient from 256 rows: its 128-row
+// tiles measured slower with 16).  The shallow stage halves the LDS of a
+// 128 x 64 tile (32 KB), so five workgroups share a CU instead of two, and
+// one workgroup's epilogue traffic overlaps the others' MFMAs (ResNet-50
+// k=2 b=32: 1x1 data gradients 147 -> 130 us, 1x1 forward 104 -> 96 us, 3x3
+// data gradients 252 -> 228 us; with the tap-major loaders the 3x3 forward
+// 211 -> 206 us).
+template <int BM, bool SP = false>
+constexpr int stage_k() { return BM >= 256 || (BM >= 128 && !SP) ? 16 : 32; }
 
 template <int BM, int BN, int WM, int WN, int R>
 hipError_t launch_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
-  constexpr int BK = stage_k<BM, R, false>();
+  constexpr int BK = stage_k<BM>();
   const int M = a.g.b * a.g.Ho * a.g.Wo;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Co, BN), a.g.k);
   if (a.g.Ci % BK == 0) {
@@ -1125,7 +1126,7 @@ hipError_t launch_fwd(const ConvFwdArgs& a, hipStream_t s, const char** name) {
 
 template <int BM, int BN, int WM, int WN, int R, int ST, bool SP = false>
 hipError_t launch_bwd_data(const ConvBwdDataArgs& a, hipStream_t s, const char** name) {
-  constexpr int BK = stage_k<BM, R, true, SP>();
+  constexpr int BK = stage_k<BM, SP>();
   const int M = SP ? a.g.b * a.g.Ho * a.g.Wo : a.g.b * a.g.H * a.g.W;
   dim3 grid(cdiv(M, BM), cdiv(a.g.Ci, BN), a.g.k);
   if constexpr (ST == 1 || SP) {
