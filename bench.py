@@ -316,7 +316,7 @@ def sma_micro(steps=20, warmup=3, repeats=5):
     ctx.close()
     del ctx, g
     torch.cuda.empty_cache()
-    la, kms, _, kby = prof["sma_k"]
+    la, kms, _, kby = next(v for n, v in prof.items() if n.startswith("sma_"))
     # a plain copy of the same size on the same box, for scale
     half = nbytes // 8
     src = torch.empty(half, dtype=torch.float32, device="cuda").fill_(1.0)

@@ -993,7 +993,7 @@ int enqueue_sma(cb_ctx* c, const float* G, int64_t gstride, int correct) {
   const double P = (double)c->p.P, k = c->p.k;
   double bytes = correct ? 4.0 * P * (3.0 * k + 4.0) : 4.0 * P * 3.0 * k;
   if (a.Wprev) bytes += 8.0 * k * P;
-  CB_LAUNCH(c, correct ? "sma_k" : "sma_k<local step>", 0.0, bytes, sma_step(a, c->stream));
+  CB_LAUNCH(c, correct ? "sma_k" : "sma_k<local step>", 0.0, bytes, sma_step(a, c->stream, &nm_));
   return CB_OK;
 }
 

@@ -360,7 +360,7 @@ struct SMAArgs {
   float alpha, lr, mu, mu_l;
   int correct;           // 0: local step only (no correction, z untouched)
 };
-hipError_t sma_step(const SMAArgs& a, hipStream_t s);
+hipError_t sma_step(const SMAArgs& a, hipStream_t s, const char** name = nullptr);
 // flag[0] = 1 if any of z[0..n) is NaN/Inf (flag must be zeroed first).
 hipError_t nonfinite_scan(const float* z, int64_t n, int* flag, hipStream_t s);
 hipError_t zero_ints(int* p, int n, hipStream_t s);

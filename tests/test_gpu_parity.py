@@ -176,7 +176,10 @@ class Pair:
 # ------------------------------------------------------------- SMA kernel
 
 SMA_CASES = [("lenet5", 1), ("lenet5", 2), ("lenet5", 3), ("lenet5", 8), ("lenet5", 32),
-             ("resnet32", 4), ("resnet32", 16), ("resnet32", 5)]
+             ("resnet32", 4), ("resnet32", 16), ("resnet32", 5),
+             # ResNet-50's P: k = 2 takes the one-column form with R = 1, k = 16 the
+             # 16-column form (ragged last block)
+             ("resnet50", 2), ("resnet50", 16)]
 MODEL_SHAPES = {"lenet5": (1, 28, 28, 10), "resnet32": (3, 32, 32, 10),
                 "resnet50": (3, 224, 224, 1000)}
 
