@@ -25,9 +25,10 @@ constexpr int C1 = 6, A1 = IMG * IMG, P1W = 14, P1 = P1W * P1W;
 constexpr int C2 = 16, A2W = 10, A2 = A2W * A2W, P2W = 5, P2 = P2W * P2W;
 constexpr int F0 = C2 * P2, F1 = 120, F2 = 84;     // 400 -> 120 -> 84 -> classes
 constexpr int NW1 = C1 * 25, NW2 = C2 * C1 * 25;   // conv weights
-constexpr int THREADS = 512;
+constexpr int THREADS = 1024;
 constexpr int D2P = A2W + 8;          // padded da2 plane width (18)
 constexpr int R1PARTS = 7, R1ROWS = IMG / R1PARTS;  // conv1 weight shares: 7 slices of 4 rows
+constexpr int D1PARTS = 4;  // conv2 data gradient: 4 quarters of the output channels
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -104,8 +105,8 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   // seven slices of conv1's weight shares
   float* const da2p = wb;
   float* const pdp1 = wb + C2 * D2P * D2P;
-  float* const part1 = pdp1 + 2 * C1 * P1;
-  static_assert(C2 * D2P * D2P + 2 * C1 * P1 + R1PARTS * (NW1 + C1) <= SLAB, "aliases fit");
+  float* const part1 = pdp1 + D1PARTS * C1 * P1;
+  static_assert(C2 * D2P * D2P + D1PARTS * C1 * P1 + R1PARTS * (NW1 + C1) <= SLAB, "aliases fit");
   const int tid = threadIdx.x;
   const int n = blockIdx.x, j = n / a.b;  // image n belongs to learner j
   const float* Wj = a.w + (int64_t)j * a.pstride;
@@ -154,23 +155,23 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     p1[o] = b;
   }
   __syncthreads();
-  for (int t0 = tid; t0 < A2 * (C2 / 4); t0 += THREADS) {  // conv2 + bias + ReLU
-    const int pix = t0 % A2, cg = t0 / A2;  // a thread per pixel and 4 output channels
+  for (int t0 = tid; t0 < A2 * (C2 / 2); t0 += THREADS) {  // conv2 + bias + ReLU
+    const int pix = t0 % A2, cg = t0 / A2;  // a thread per pixel and 2 output channels
     const int y = pix / A2W, xx = pix % A2W;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc[2] = {0.f, 0.f};
     for (int c = 0; c < C1; ++c) {
       float v[25];
 #pragma unroll
       for (int t = 0; t < 25; ++t) v[t] = p1[c * P1 + (y + t / 5) * P1W + xx + t % 5];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int t = 0; t < 25; ++t) acc[u] += w2[(cg * 4 + u) * 150 + c * 25 + t] * v[t];
+        for (int t = 0; t < 25; ++t) acc[u] += w2[(cg * 2 + u) * 150 + c * 25 + t] * v[t];
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float s = acc[u] + b2[cg * 4 + u];
-      a2[(cg * 4 + u) * A2 + pix] = s > 0.f ? s : 0.f;
+    for (int u = 0; u < 2; ++u) {
+      const float s = acc[u] + b2[cg * 2 + u];
+      a2[(cg * 2 + u) * A2 + pix] = s > 0.f ? s : 0.f;
     }
   }
   __syncthreads();
@@ -249,13 +250,14 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   }
   __syncthreads();
   // conv2 data gradient: dp1[c][iy][ix] = sum over co, r, q of
-  // da2[co][iy - r][ix - q] w2[co][c][r][q]; a thread per input pixel and half
-  // of the output channels, all six input channels; the halves summed in order
-  for (int t0 = tid; t0 < 2 * P1; t0 += THREADS) {
-    const int pix = t0 % P1, half = t0 / P1;
+  // da2[co][iy - r][ix - q] w2[co][c][r][q]; a thread per input pixel and a
+  // quarter of the output channels, all six input channels; the quarters
+  // summed in order
+  for (int t0 = tid; t0 < D1PARTS * P1; t0 += THREADS) {
+    const int pix = t0 % P1, qt = t0 / P1;
     const int iy = pix / P1W + 4, ix = pix % P1W + 4;
     float acc[C1] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int co = half * (C2 / 2); co < (half + 1) * (C2 / 2); ++co) {
+    for (int co = qt * (C2 / D1PARTS); co < (qt + 1) * (C2 / D1PARTS); ++co) {
       float v[25];
 #pragma unroll
       for (int t = 0; t < 25; ++t) v[t] = da2p[co * D2P * D2P + (iy - t / 5) * D2P + ix - t % 5];
@@ -265,10 +267,11 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
         for (int t = 0; t < 25; ++t) acc[c] += w2[co * 150 + c * 25 + t] * v[t];
     }
 #pragma unroll
-    for (int c = 0; c < C1; ++c) pdp1[half * C1 * P1 + c * P1 + pix] = acc[c];
+    for (int c = 0; c < C1; ++c) pdp1[qt * C1 * P1 + c * P1 + pix] = acc[c];
   }
   __syncthreads();
-  for (int e = tid; e < C1 * P1; e += THREADS) dp1[e] = pdp1[e] + pdp1[C1 * P1 + e];
+  for (int e = tid; e < C1 * P1; e += THREADS)
+    dp1[e] = ((pdp1[e] + pdp1[C1 * P1 + e]) + pdp1[2 * C1 * P1 + e]) + pdp1[3 * C1 * P1 + e];
   __syncthreads();
   for (int e = tid; e < C1 * A1; e += THREADS) {  // pool1 backward, ReLU mask (in a1)
     const int c = e / A1, y = (e % A1) / IMG, xx = e % IMG;
