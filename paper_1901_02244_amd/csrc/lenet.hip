@@ -370,7 +370,16 @@ __global__ __launch_bounds__(256) void lenet_learner_k(LenetArgs a) {
     // (one parameter per thread: the grid covers P)
     float s = 0.f;
     if (e < LENET_CONV_PARAMS) {
-      for (int i = 0; i < a.b; ++i) s += cw[(int64_t)i * LENET_CONV_PARAMS + e];
+      // eight images' shares in flight at a time, added in image order
+      for (int i0 = 0; i0 < a.b; i0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          v[u] = i0 + u < a.b ? cw[(int64_t)(i0 + u) * LENET_CONV_PARAMS + e] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (i0 + u < a.b) s += v[u];
+      }
     } else {
       // dW[o][in] = sum over images of dy[o] * x[in]; db[o] = sum of dy[o]
       int dyo, xo = -1;
@@ -380,9 +389,19 @@ __global__ __launch_bounds__(256) void lenet_learner_k(LenetArgs a) {
       else if (e < o_fw3) { dyo = LENET_DF2 + (int)(e - o_fb2); }
       else if (e < o_fb3) { dyo = LENET_DL + (int)((e - o_fw3) / F2); xo = LENET_F2 + (int)((e - o_fw3) % F2); }
       else { dyo = LENET_DL + (int)(e - o_fb3); }
-      for (int i = 0; i < a.b; ++i) {
-        const float* v = fv + (int64_t)i * LENET_FC_VEC;
-        s += xo >= 0 ? v[dyo] * v[xo] : v[dyo];
+      // eight images' terms in flight at a time, added in image order
+      for (int i0 = 0; i0 < a.b; i0 += 8) {
+        float dy[8], xv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float* v = fv + (int64_t)(i0 + u) * LENET_FC_VEC;
+          const bool in = i0 + u < a.b;
+          dy[u] = in ? v[dyo] : 0.f;
+          xv[u] = in && xo >= 0 ? v[xo] : 1.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (i0 + u < a.b) s += xo >= 0 ? dy[u] * xv[u] : dy[u];
       }
     }
     g[e] = s;
