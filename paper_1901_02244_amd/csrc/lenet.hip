@@ -60,21 +60,27 @@ __device__ __forceinline__ int win_arg(float v0, float v1, float v2, float v3, f
 constexpr int SLAB_ROWS = 40, SLAB = SLAB_ROWS * F0;  // 16000 floats (64 KB)
 static_assert(F2 * F1 <= SLAB && LENET_MAX_CLASSES * F2 <= SLAB, "FC weights fit the slab");
 
-// dst[0, n) = src[0, n); n a multiple of 4, src 16-byte aligned.
-__device__ __forceinline__ void stage(float* dst, const float* src, int n) {
+// A slab is copied in two halves, with 16-byte loads (n a multiple of 4, src
+// 16-byte aligned): fetch issues the global reads into registers (at most PFQ
+// float4s a thread) and put writes them to LDS later, so that a slab's reads
+// overlap the work before its use (the first slab's the convolutions, each
+// later one's the use of the slab before it).
+constexpr int PFQ = (SLAB / 4 + THREADS - 1) / THREADS;
+__device__ __forceinline__ void fetch(v4f (&r)[PFQ], const float* src, int n) {
   const v4f* s4 = reinterpret_cast<const v4f*>(src);
-  v4f* d4 = reinterpret_cast<v4f*>(dst);
-  const int n4 = n >> 2;
-  int e = threadIdx.x;
-#pragma unroll 4
-  for (; e + 3 * THREADS < n4; e += 4 * THREADS) {
-    const v4f a0 = s4[e], a1 = s4[e + THREADS], a2 = s4[e + 2 * THREADS], a3 = s4[e + 3 * THREADS];
-    d4[e] = a0;
-    d4[e + THREADS] = a1;
-    d4[e + 2 * THREADS] = a2;
-    d4[e + 3 * THREADS] = a3;
+#pragma unroll
+  for (int u = 0; u < PFQ; ++u) {
+    const int e = threadIdx.x + u * THREADS;
+    if (e < (n >> 2)) r[u] = s4[e];
   }
-  for (; e < n4; e += THREADS) d4[e] = s4[e];
+}
+__device__ __forceinline__ void put(float* dst, const v4f (&r)[PFQ], int n) {
+  v4f* d4 = reinterpret_cast<v4f*>(dst);
+#pragma unroll
+  for (int u = 0; u < PFQ; ++u) {
+    const int e = threadIdx.x + u * THREADS;
+    if (e < (n >> 2)) d4[e] = r[u];
+  }
 }
 
 // y[o0 + r] = bias[o0 + r] + sum_i W[r][i] x[i] for the nrows rows of W in
@@ -131,6 +137,8 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     else if (e < NW1 + C1 + NW2) w2[e - NW1 - C1] = v;
     else b2[e - NW1 - C1 - NW2] = v;
   }
+  v4f pf[PFQ];
+  fetch(pf, fw1, SLAB);  // FC1's first slab, in flight through the convolutions
   __syncthreads();
   for (int pix = tid; pix < A1; pix += THREADS) {  // conv1 + bias + ReLU, a thread per pixel
     const int y = pix / IMG, xx = pix % IMG;
@@ -184,17 +192,22 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   }
   __syncthreads();
   for (int o0 = 0; o0 < F1; o0 += SLAB_ROWS) {  // FC1 + ReLU, by slabs
-    stage(wb, fw1 + o0 * F0, SLAB);
+    put(wb, pf, SLAB);
     __syncthreads();
+    // the next slab (or W2) is read while this one is used
+    if (o0 + SLAB_ROWS < F1) fetch(pf, fw1 + (o0 + SLAB_ROWS) * F0, SLAB);
+    else fetch(pf, fw2, F2 * F1);
     fc_rows(wb, fb1, p2, F0, o0, SLAB_ROWS, true, f1);
     __syncthreads();
   }
-  stage(wb, fw2, F2 * F1);  // FC2 + ReLU
+  put(wb, pf, F2 * F1);  // FC2 + ReLU
   __syncthreads();
+  fetch(pf, fw3, C * F2);
   fc_rows(wb, fb2, f1, F1, 0, F2, true, f2);
   __syncthreads();
-  stage(wb, fw3, C * F2);  // FC3 (kept in LDS for its data gradient)
+  put(wb, pf, C * F2);  // FC3 (kept in LDS for its data gradient)
   __syncthreads();
+  fetch(pf, fw2, F2 * F1);  // for the backward pass
   fc_rows(wb, fb3, f2, F2, 0, C, false, lg);
   __syncthreads();
   // softmax cross-entropy of this image: the loss term and (softmax -
@@ -218,8 +231,9 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     df2[i] = f2[i] > 0.f ? s : 0.f;
   }
   __syncthreads();
-  stage(wb, fw2, F2 * F1);
+  put(wb, pf, F2 * F1);
   __syncthreads();
+  fetch(pf, fw1, SLAB);
   for (int i = tid; i < F1; i += THREADS) {
     float s = 0.f;
     for (int o = 0; o < F2; ++o) s += df2[o] * wb[o * F1 + i];
@@ -228,8 +242,9 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   for (int i = tid; i < F0; i += THREADS) dp2[i] = 0.f;
   for (int o0 = 0; o0 < F1; o0 += SLAB_ROWS) {  // dp2 = W1^T df1, slab by slab in order
     __syncthreads();
-    stage(wb, fw1 + o0 * F0, SLAB);
+    put(wb, pf, SLAB);
     __syncthreads();
+    if (o0 + SLAB_ROWS < F1) fetch(pf, fw1 + (o0 + SLAB_ROWS) * F0, SLAB);
     for (int i = tid; i < F0; i += THREADS) {
       float s = dp2[i];
       for (int r = 0; r < SLAB_ROWS; ++r) s += df1[o0 + r] * wb[r * F0 + i];
