@@ -103,6 +103,7 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   __shared__ float a2[C2 * A2], p2[F0];
   __shared__ unsigned char g1[C1 * P1], g2[F0];
   __shared__ float f1[F1], f2[F2], lg[LENET_MAX_CLASSES];
+  __shared__ float fbs[F1 + F2 + LENET_MAX_CLASSES];  // the FC biases
   __shared__ float dl[LENET_MAX_CLASSES], df2[F2], df1[F1], dp2[F0];
   __shared__ float da2[C2 * A2], dp1[C1 * P1];
   __shared__ __attribute__((aligned(16))) float wb[SLAB];
@@ -137,6 +138,10 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     else if (e < NW1 + C1 + NW2) w2[e - NW1 - C1] = v;
     else b2[e - NW1 - C1 - NW2] = v;
   }
+  // the FC biases and the label are read here too, off the FC chain
+  for (int e = tid; e < F1 + F2 + C; e += THREADS)
+    fbs[e] = e < F1 ? fb1[e] : (e < F1 + F2 ? fb2[e - F1] : fb3[e - F1 - F2]);
+  const int label = a.labels[n];
   v4f pf[PFQ];
   fetch(pf, fw1, SLAB);  // FC1's first slab, in flight through the convolutions
   __syncthreads();
@@ -197,23 +202,22 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     // the next slab (or W2) is read while this one is used
     if (o0 + SLAB_ROWS < F1) fetch(pf, fw1 + (o0 + SLAB_ROWS) * F0, SLAB);
     else fetch(pf, fw2, F2 * F1);
-    fc_rows(wb, fb1, p2, F0, o0, SLAB_ROWS, true, f1);
+    fc_rows(wb, fbs, p2, F0, o0, SLAB_ROWS, true, f1);
     __syncthreads();
   }
   put(wb, pf, F2 * F1);  // FC2 + ReLU
   __syncthreads();
   fetch(pf, fw3, C * F2);
-  fc_rows(wb, fb2, f1, F1, 0, F2, true, f2);
+  fc_rows(wb, fbs + F1, f1, F1, 0, F2, true, f2);
   __syncthreads();
   put(wb, pf, C * F2);  // FC3 (kept in LDS for its data gradient)
   __syncthreads();
   fetch(pf, fw2, F2 * F1);  // for the backward pass
-  fc_rows(wb, fb3, f2, F2, 0, C, false, lg);
+  fc_rows(wb, fbs + F1 + F2, f2, F2, 0, C, false, lg);
   __syncthreads();
   // softmax cross-entropy of this image: the loss term and (softmax -
   // onehot) / b; a label out of range gives a NaN term and no one-hot
   if (tid < 64) {
-    const int label = a.labels[n];
     const bool on = tid < C;
     const float o = on ? lg[tid] : -INFINITY;
     const float mx = wave_max(o);
