@@ -31,6 +31,10 @@ constexpr int R1PARTS = 7, R1ROWS = IMG / R1PARTS;  // conv1 weight shares: 7 sl
 constexpr int D1PARTS = 4;  // conv2 data gradient: 4 quarters of the output channels
 typedef float v4f __attribute__((ext_vector_type(4)));
 
+__device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -104,6 +108,10 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   __shared__ unsigned char g1[C1 * P1], g2[F0];
   __shared__ float f1[F1], f2[F2], lg[LENET_MAX_CLASSES];
   __shared__ float fbs[F1 + F2 + LENET_MAX_CLASSES];  // the FC biases
+  __shared__ int koff2[NW2 / C2];  // conv2 tap k = (c, r, s): its offset in p1
+  // conv2's filters again as [co][tap][8 input channels, 6 used]: the data
+  // gradient reads a tap's six weights as two vector loads
+  __shared__ __attribute__((aligned(16))) float w2t[C2 * 25 * 8];
   __shared__ float dl[LENET_MAX_CLASSES], df2[F2], df1[F1], dp2[F0];
   __shared__ float da2[C2 * A2], dp1[C1 * P1];
   __shared__ __attribute__((aligned(16))) float wb[SLAB];
@@ -135,12 +143,18 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     const float v = Wj[e];
     if (e < NW1) w1[e] = v;
     else if (e < NW1 + C1) b1[e - NW1] = v;
-    else if (e < NW1 + C1 + NW2) w2[e - NW1 - C1] = v;
+    else if (e < NW1 + C1 + NW2) {
+      const int f = e - NW1 - C1;
+      w2[f] = v;
+      w2t[((f / 150) * 25 + f % 25) * 8 + (f % 150) / 25] = v;
+    }
     else b2[e - NW1 - C1 - NW2] = v;
   }
   // the FC biases and the label are read here too, off the FC chain
   for (int e = tid; e < F1 + F2 + C; e += THREADS)
     fbs[e] = e < F1 ? fb1[e] : (e < F1 + F2 ? fb2[e - F1] : fb3[e - F1 - F2]);
+  for (int e = tid; e < NW2 / C2; e += THREADS)
+    koff2[e] = (e / 25) * P1 + ((e % 25) / 5) * P1W + e % 5;
   const int label = a.labels[n];
   v4f pf[PFQ];
   fetch(pf, fw1, SLAB);  // FC1's first slab, in flight through the convolutions
@@ -168,23 +182,28 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     p1[o] = b;
   }
   __syncthreads();
-  for (int t0 = tid; t0 < A2 * (C2 / 2); t0 += THREADS) {  // conv2 + bias + ReLU
-    const int pix = t0 % A2, cg = t0 / A2;  // a thread per pixel and 2 output channels
-    const int y = pix / A2W, xx = pix % A2W;
-    float acc[2] = {0.f, 0.f};
-    for (int c = 0; c < C1; ++c) {
-      float v[25];
-#pragma unroll
-      for (int t = 0; t < 25; ++t) v[t] = p1[c * P1 + (y + t / 5) * P1W + xx + t % 5];
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int t = 0; t < 25; ++t) acc[u] += w2[(cg * 2 + u) * 150 + c * 25 + t] * v[t];
+  // conv2 + bias + ReLU on fp32 MFMA: rows = the 100 output pixels (7 tiles
+  // of 16, a wave each), columns = the 16 output channels, contraction over
+  // the 150 taps k = (c, r, s) in 38 steps of 4 (k >= 150 reads 0)
+  if ((tid >> 6) < (A2 + 15) / 16) {
+    constexpr int K2 = NW2 / C2;
+    const int lane = tid & 63, tile = tid >> 6;
+    const int m = tile * 16 + (lane & 15), co = lane & 15, kq = lane >> 4;
+    const bool mok = m < A2;
+    const int pb = mok ? (m / A2W) * P1W + m % A2W : 0;
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < (K2 + 3) / 4; ++t) {
+      const int k = 4 * t + kq;
+      const bool kok = k < K2;
+      const float av = (mok && kok) ? p1[pb + koff2[k]] : 0.f;
+      const float bv = kok ? w2[co * K2 + k] : 0.f;
+      acc = mfma4(av, bv, acc);
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const float s = acc[u] + b2[cg * 2 + u];
-      a2[(cg * 2 + u) * A2 + pix] = s > 0.f ? s : 0.f;
+    for (int i = 0; i < 4; ++i) {
+      const int mm = tile * 16 + kq * 4 + i;
+      const float s = acc[i] + b2[co];
+      if (mm < A2) a2[co * A2 + mm] = s > 0.f ? s : 0.f;
     }
   }
   __syncthreads();
@@ -281,9 +300,15 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
 #pragma unroll
       for (int t = 0; t < 25; ++t) v[t] = da2p[co * D2P * D2P + (iy - t / 5) * D2P + ix - t % 5];
 #pragma unroll
-      for (int c = 0; c < C1; ++c)
+      for (int t = 0; t < 25; ++t) {
+        const float* wt = w2t + (co * 25 + t) * 8;
+        const v4f wa = *reinterpret_cast<const v4f*>(wt);
+        const v4f wc = *reinterpret_cast<const v4f*>(wt + 4);
 #pragma unroll
-        for (int t = 0; t < 25; ++t) acc[c] += w2[co * 150 + c * 25 + t] * v[t];
+        for (int c = 0; c < 4; ++c) acc[c] += wa[c] * v[t];
+        acc[4] += wc[0] * v[t];
+        acc[5] += wc[1] * v[t];
+      }
     }
 #pragma unroll
     for (int c = 0; c < C1; ++c) pdp1[qt * C1 * P1 + c * P1 + pix] = acc[c];
