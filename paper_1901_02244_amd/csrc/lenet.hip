@@ -28,7 +28,7 @@ constexpr int NW1 = C1 * 25, NW2 = C2 * C1 * 25;   // conv weights
 constexpr int THREADS = 1024;
 constexpr int D2P = A2W + 8;          // padded da2 plane width (18)
 constexpr int R1PARTS = 7, R1ROWS = IMG / R1PARTS;  // conv1 weight shares: 7 slices of 4 rows
-constexpr int D1PARTS = 4;  // conv2 data gradient: 4 quarters of the output channels
+constexpr int D1PARTS = 8;  // conv2 data gradient: 8 parts of the output channels
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
@@ -288,34 +288,52 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   }
   __syncthreads();
   // conv2 data gradient: dp1[c][iy][ix] = sum over co, r, q of
-  // da2[co][iy - r][ix - q] w2[co][c][r][q]; a thread per input pixel and a
-  // quarter of the output channels, all six input channels; the quarters
-  // summed in order
-  for (int t0 = tid; t0 < D1PARTS * P1; t0 += THREADS) {
-    const int pix = t0 % P1, qt = t0 / P1;
-    const int iy = pix / P1W + 4, ix = pix % P1W + 4;
-    float acc[C1] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  // da2[co][iy - r][ix - q] w2[co][c][r][q]; a thread per pair of
+  // horizontally adjacent input pixels and an eighth of the output
+  // channels, all six input channels, so that the pair shares its 5 x 6
+  // window reads and each tap's weight loads; the eighths summed in order
+  for (int t0 = tid; t0 < D1PARTS * (P1 / 2); t0 += THREADS) {
+    const int pp = t0 % (P1 / 2), qt = t0 / (P1 / 2);
+    const int iy = pp / (P1W / 2) + 4, ix = 2 * (pp % (P1W / 2)) + 4;
+    float acc0[C1] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, acc1[C1] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int co = qt * (C2 / D1PARTS); co < (qt + 1) * (C2 / D1PARTS); ++co) {
-      float v[25];
+      float v[5][6];  // da2 rows iy - r, columns ix - 4 .. ix + 1
 #pragma unroll
-      for (int t = 0; t < 25; ++t) v[t] = da2p[co * D2P * D2P + (iy - t / 5) * D2P + ix - t % 5];
+      for (int r = 0; r < 5; ++r)
+#pragma unroll
+        for (int u = 0; u < 6; ++u) v[r][u] = da2p[co * D2P * D2P + (iy - r) * D2P + ix - 4 + u];
 #pragma unroll
       for (int t = 0; t < 25; ++t) {
+        const int r = t / 5, q = t % 5;
         const float* wt = w2t + (co * 25 + t) * 8;
         const v4f wa = *reinterpret_cast<const v4f*>(wt);
         const v4f wc = *reinterpret_cast<const v4f*>(wt + 4);
+        const float x0 = v[r][4 - q], x1 = v[r][5 - q];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[c] += wa[c] * v[t];
-        acc[4] += wc[0] * v[t];
-        acc[5] += wc[1] * v[t];
+        for (int c = 0; c < 4; ++c) {
+          acc0[c] += wa[c] * x0;
+          acc1[c] += wa[c] * x1;
+        }
+        acc0[4] += wc[0] * x0;
+        acc0[5] += wc[1] * x0;
+        acc1[4] += wc[0] * x1;
+        acc1[5] += wc[1] * x1;
       }
     }
+    const int pix = (iy - 4) * P1W + ix - 4;
 #pragma unroll
-    for (int c = 0; c < C1; ++c) pdp1[qt * C1 * P1 + c * P1 + pix] = acc[c];
+    for (int c = 0; c < C1; ++c) {
+      pdp1[qt * C1 * P1 + c * P1 + pix] = acc0[c];
+      pdp1[qt * C1 * P1 + c * P1 + pix + 1] = acc1[c];
+    }
   }
   __syncthreads();
-  for (int e = tid; e < C1 * P1; e += THREADS)
-    dp1[e] = ((pdp1[e] + pdp1[C1 * P1 + e]) + pdp1[2 * C1 * P1 + e]) + pdp1[3 * C1 * P1 + e];
+  for (int e = tid; e < C1 * P1; e += THREADS) {
+    float s = pdp1[e];
+#pragma unroll
+    for (int q = 1; q < D1PARTS; ++q) s += pdp1[q * C1 * P1 + e];
+    dp1[e] = s;
+  }
   __syncthreads();
   for (int e = tid; e < C1 * A1; e += THREADS) {  // pool1 backward, ReLU mask (in a1)
     const int c = e / A1, y = (e % A1) / IMG, xx = e % IMG;
