@@ -970,7 +970,6 @@ __global__ __launch_bounds__(64 * FCM_WAVES) void fc_fwd_mfma_k(const float* x, 
   v4f acc[MF];
 #pragma unroll
   for (int f = 0; f < MF; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
   for (int g = g0; g < g1; ++g) {
     const int k = g * 16 + q;  // the lane's first step
     v4f av[MF];
@@ -1020,7 +1019,6 @@ __global__ __launch_bounds__(64 * FCM_WAVES) void fc_dgrad_mfma_k(const float* d
   v4f acc[MF];
 #pragma unroll
   for (int f = 0; f < MF; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
   for (int g = g0; g < g1; ++g) {
     const int k = g * 16 + q;  // the lane's first output channel
     v4f av[MF];
