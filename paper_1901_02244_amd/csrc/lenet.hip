@@ -91,12 +91,21 @@ __device__ __forceinline__ void put(float* dst, const v4f (&r)[PFQ], int n) {
 // LDS (row length nin), a wave per row, lanes over the inputs; ReLU if relu.
 __device__ __forceinline__ void fc_rows(const float* W, const float* bias, const float* x, int nin,
                                         int o0, int nrows, bool relu, float* y) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  for (int r = w; r < nrows; r += THREADS / 64) {
+  // 16 lanes per row, four rows per wave at a time: lane l of a row sums the
+  // inputs l, l + 16, ... in order, then a 16-lane xor butterfly combines
+  // the lanes (4 steps instead of a 64-lane sum's 6, for four rows at once)
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, l16 = lane & 15;
+  for (int r0 = w * 4; r0 < nrows; r0 += THREADS / 16) {
+    const int r = r0 + (lane >> 4);
     float s = 0.f;
-    for (int i = lane; i < nin; i += 64) s += W[r * nin + i] * x[i];
-    s = wave_sum(s) + bias[o0 + r];
-    if (lane == 0) y[o0 + r] = relu ? (s > 0.f ? s : 0.f) : s;
+    if (r < nrows)
+      for (int i = l16; i < nin; i += 16) s += W[r * nin + i] * x[i];
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 16);
+    if (l16 == 0 && r < nrows) {
+      s += bias[o0 + r];
+      y[o0 + r] = relu ? (s > 0.f ? s : 0.f) : s;
+    }
   }
 }
 
