@@ -268,16 +268,25 @@ def lenet_latency(iters=1000, repeats=5):
                       "images_per_s": round(small.n_images / ms2 * 1e3, 1), "iterations": 10}}
 
 
-def resnet50_throughput(steps=20, warmup=3, repeats=5):
+def resnet50_throughput(steps=20, warmup=3, repeats=5, prof_steps=0):
     """ResNet-50, k = 2 learners of 32 images at 224 x 224: images/s (median
-    of `repeats` runs of `steps` iterations)."""
+    of `repeats` runs of `steps` iterations); with prof_steps, also each
+    kernel's duration in that many instrumented iterations."""
     import workloads as wl
 
     wk = wl.RESNET50_K2
-    ms, _, _ = time_training(wk, steps, warmup, ring=2, repeats=repeats)
+    r = time_training(wk, steps, warmup, ring=2, prof_steps=prof_steps, repeats=repeats)
+    ms = r[0]
     log(f"[bench] ResNet-50 k=2 b=32: {ms:.2f} ms/iteration, {wk.n_images / ms * 1e3:.0f} images/s")
-    return {"ms_per_iteration": round(ms, 3), "images_per_s": round(wk.n_images / ms * 1e3, 1),
-            "steps": steps, "repeats": repeats}
+    out = {"ms_per_iteration": round(ms, 3), "images_per_s": round(wk.n_images / ms * 1e3, 1),
+           "steps": steps, "repeats": repeats}
+    if prof_steps:
+        out["kernels_per_iteration"] = {
+            k: {"launches": v[0], "ms": round(v[1], 4),
+                **({"TFLOP/s": round(v[2] / (v[1] * 1e-3) / 1e12, 2)} if v[2] else {}),
+                "GB/s": round(v[3] / (v[1] * 1e-3) / 1e9, 1)}
+            for k, v in sorted(r[3].items(), key=lambda kv: -kv[1][1])}
+    return out
 
 
 def sma_micro(steps=20, warmup=3, repeats=5):
@@ -475,6 +484,8 @@ def main():
                     help="timed runs of the headline workload; the median is reported")
     ap.add_argument("--only", choices=("lenet", "resnet50", "sma"),
                     help="run only this workload (for profiling) and print its figures")
+    ap.add_argument("--kernels", action="store_true",
+                    help="with --only resnet50: also each kernel's duration in 3 instrumented iterations")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="first run one plain copy kernel of this many MiB (read and written once "
                          "each), the reference dispatch for HBM byte counters")
@@ -500,7 +511,8 @@ def main():
         torch.cuda.empty_cache()
     if args.only:
         fn = {"lenet": lenet_latency, "resnet50": resnet50_throughput, "sma": sma_micro}[args.only]
-        print(json.dumps({"only": args.only, **fn()}), flush=True)
+        res = resnet50_throughput(prof_steps=3) if args.only == "resnet50" and args.kernels else fn()
+        print(json.dumps({"only": args.only, **res}), flush=True)
         return
     wk = wl.RESNET32_K4
     log(f"[bench] {wk.name}: warmup {args.warmup}, steps {args.steps} x {args.repeats} repeats")
