@@ -88,18 +88,34 @@ __device__ __forceinline__ void put(float* dst, const v4f (&r)[PFQ], int n) {
 }
 
 // y[o0 + r] = bias[o0 + r] + sum_i W[r][i] x[i] for the nrows rows of W in
-// LDS (row length nin), a wave per row, lanes over the inputs; ReLU if relu.
-__device__ __forceinline__ void fc_rows(const float* W, const float* bias, const float* x, int nin,
-                                        int o0, int nrows, bool relu, float* y) {
-  // 16 lanes per row, four rows per wave at a time: lane l of a row sums the
-  // inputs l, l + 16, ... in order, then a 16-lane xor butterfly combines
-  // the lanes (4 steps instead of a 64-lane sum's 6, for four rows at once)
+// LDS (row length NIN, 16-byte aligned rows and x); ReLU if relu.
+template <int NIN>
+__device__ __forceinline__ void fc_rows(const float* W, const float* bias, const float* x, int o0,
+                                        int nrows, bool relu, float* y) {
+  // 16 lanes per row, four rows per wave at a time: lane l of a row takes the
+  // input quads l, l + 16, ..., reads all of them and their weights first,
+  // then sums the inputs in that order; a 16-lane xor butterfly combines the
+  // lanes (4 steps instead of a 64-lane sum's 6, for four rows at once)
+  static_assert(NIN % 4 == 0, "rows of whole quads");
+  constexpr int NQ = NIN / 4, NQL = (NQ + 15) / 16;  // quads per row, per lane
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, l16 = lane & 15;
   for (int r0 = w * 4; r0 < nrows; r0 += THREADS / 16) {
     const int r = r0 + (lane >> 4);
     float s = 0.f;
-    if (r < nrows)
-      for (int i = l16; i < nin; i += 16) s += W[r * nin + i] * x[i];
+    if (r < nrows) {
+      v4f wv[NQL], xv[NQL];
+#pragma unroll
+      for (int i = 0; i < NQL; ++i)
+        if (l16 + 16 * i < NQ) {
+          wv[i] = *reinterpret_cast<const v4f*>(W + r * NIN + 4 * (l16 + 16 * i));
+          xv[i] = *reinterpret_cast<const v4f*>(x + 4 * (l16 + 16 * i));
+        }
+#pragma unroll
+      for (int i = 0; i < NQL; ++i)
+        if (l16 + 16 * i < NQ)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) s += wv[i][c] * xv[i][c];
+    }
 #pragma unroll
     for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 16);
     if (l16 == 0 && r < nrows) {
@@ -113,9 +129,12 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
   __shared__ float xs[PADW * PADW];
   __shared__ float w1[NW1], b1[C1], w2[NW2], b2[C2];
   __shared__ float a1[C1 * A1], p1[C1 * P1];
-  __shared__ float a2[C2 * A2], p2[F0];
+  __shared__ float a2[C2 * A2];
+  __shared__ __attribute__((aligned(16))) float p2[F0];
   __shared__ unsigned char g1[C1 * P1], g2[F0];
-  __shared__ float f1[F1], f2[F2], lg[LENET_MAX_CLASSES];
+  __shared__ __attribute__((aligned(16))) float f1[F1];
+  __shared__ __attribute__((aligned(16))) float f2[F2];
+  __shared__ float lg[LENET_MAX_CLASSES];
   __shared__ float fbs[F1 + F2 + LENET_MAX_CLASSES];  // the FC biases
   __shared__ int koff2[NW2 / C2];  // conv2 tap k = (c, r, s): its offset in p1
   // conv2's filters again as [co][tap][8 input channels, 6 used]: the data
@@ -230,18 +249,18 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     // the next slab (or W2) is read while this one is used
     if (o0 + SLAB_ROWS < F1) fetch(pf, fw1 + (o0 + SLAB_ROWS) * F0, SLAB);
     else fetch(pf, fw2, F2 * F1);
-    fc_rows(wb, fbs, p2, F0, o0, SLAB_ROWS, true, f1);
+    fc_rows<F0>(wb, fbs, p2, o0, SLAB_ROWS, true, f1);
     __syncthreads();
   }
   put(wb, pf, F2 * F1);  // FC2 + ReLU
   __syncthreads();
   fetch(pf, fw3, C * F2);
-  fc_rows(wb, fbs + F1, f1, F1, 0, F2, true, f2);
+  fc_rows<F1>(wb, fbs + F1, f1, 0, F2, true, f2);
   __syncthreads();
   put(wb, pf, C * F2);  // FC3 (kept in LDS for its data gradient)
   __syncthreads();
   fetch(pf, fw2, F2 * F1);  // for the backward pass
-  fc_rows(wb, fbs + F1 + F2, f2, F2, 0, C, false, lg);
+  fc_rows<F2>(wb, fbs + F1 + F2, f2, 0, C, false, lg);
   __syncthreads();
   // softmax cross-entropy of this image: the loss term and (softmax -
   // onehot) / b; a label out of range gives a NaN term and no one-hot
