@@ -220,12 +220,22 @@ __global__ __launch_bounds__(THREADS) void lenet_image_k(LenetArgs a) {
     const bool mok = m < A2;
     const int pb = mok ? (m / A2W) * P1W + m % A2W : 0;
     v4f acc = {0.f, 0.f, 0.f, 0.f};
-    for (int t = 0; t < (K2 + 3) / 4; ++t) {
-      const int k = 4 * t + kq;
-      const bool kok = k < K2;
-      const float av = (mok && kok) ? p1[pb + koff2[k]] : 0.f;
-      const float bv = kok ? w2[co * K2 + k] : 0.f;
-      acc = mfma4(av, bv, acc);
+    // ten steps' operands read before their MFMAs, so that their LDS
+    // reads (the tap table, then the input) are in flight together
+    constexpr int NT2 = (K2 + 3) / 4, BT = 10;
+    for (int t0 = 0; t0 < NT2; t0 += BT) {
+      float av[BT], bv[BT];
+#pragma unroll
+      for (int u = 0; u < BT; ++u) {
+        const int k = 4 * (t0 + u) + kq;
+        const bool kok = k < K2;
+        const int kc = kok ? k : 0;
+        av[u] = (mok && kok) ? p1[pb + koff2[kc]] : 0.f;
+        bv[u] = kok ? w2[co * K2 + kc] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < BT; ++u)
+        if (t0 + u < NT2) acc = mfma4(av[u], bv[u], acc);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
