@@ -357,6 +357,23 @@ def test_lenet_k2_b4_ten_iterations():
     assert err <= TOL_Z_L2
 
 
+@pytest.mark.parametrize("classes", [1, 64])
+def test_lenet_fused_class_count_extremes(classes):
+    """The fused LeNet path at its smallest and largest class counts (one
+    class: every logit gradient is exactly zero, so is every gradient;
+    64 classes: the FC3 rows fill one pass of the FC kernel and the softmax
+    a whole wave): two SMA iterations, every gradient and update at 1e-4
+    per tensor."""
+    p = Pair("lenet5", 1, 28, 28, classes, k=2, b=4, seed=3, tag=f"lenet5 {classes} classes")
+    for t in range(2):
+        p.step(t)
+        p.check_grads(verbose=t == 0)
+        p.sync(verbose=t == 0)
+    err = p.z_error()
+    p.summary(f"z rel-L2 after 2 {err:.2e}")
+    assert err <= TOL_Z_L2
+
+
 def test_lenet_k8_b16_hundred_iterations():
     """LeNet, 8 learners of 16, 100 SMA iterations with every step's
     gradients and updates at 1e-4 per tensor; z within 1e-3 after 10 and
